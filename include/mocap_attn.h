@@ -1,0 +1,185 @@
+/*
+ * mocap_attn.h -- C ABI of libmocap_attn: chunked causal prefill attention on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (MOCAP, Section 2.2 "Chunked Pipeline", and Eq. (1) of
+ * Section 3.2): a long prompt of S tokens is cut into chunks; chunk c has
+ * L_c query tokens and sits behind a prefix of P_c = L_1 + ... + L_{c-1}
+ * tokens.  Its queries attend to the keys/values of every earlier chunk (the
+ * prefix, no mask) and to its own keys under a causal mask, so chunk c costs
+ * about L_c (P_c + L_c) -- the growth with P_c that the paper's
+ * latency-balanced chunk partitioning (Section 4.2) compensates.  The
+ * keys/values of earlier chunks stay resident between chunks; the paper's
+ * memory-balanced KV reallocation (Section 4.1) moves part of them elsewhere,
+ * which is why this library addresses them through a block table rather than
+ * assuming one contiguous buffer.
+ *
+ * For query row i of chunk c (absolute position t = P_c + i), head h:
+ *   kvh   = h / (h_q / h_kv)                      contiguous GQA groups
+ *   s_j   = scale * <q_{i,h}, k_{j,kvh}>          for keys j = 0 .. t
+ *   lse   = ln( sum_j exp(s_j) )
+ *   o_i,h = sum_j exp(s_j - lse) * v_{j,kvh}
+ * Inputs are bf16; products accumulate in fp32; softmax runs in fp32; the
+ * probabilities are rounded to bf16 before the P*V product; O is rounded to
+ * bf16 (round to nearest even); LSE is fp32.
+ *
+ * Conventions shared by every call
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     allocates no memory and keeps no state across calls except a per-device
+ *     cache of the compute-unit count.
+ *   - Calls enqueue work on `stream` (a hipStream_t passed as void*; NULL is
+ *     the default stream) and return without synchronising.  A device-side
+ *     fault shows up at the caller's next synchronisation.
+ *   - Arguments are validated on the host before anything is enqueued; on any
+ *     error status nothing is launched and nothing is written.
+ *   - Position p of the sequence lives in logical block p / block_size at
+ *     slot p % block_size; block_table[logical] gives the physical block.
+ *     Table entries are trusted: each must lie in [0, num_blocks), and
+ *     distinct positions must not share a slot.
+ *   - All device pointers must be 16-byte aligned.
+ */
+#ifndef MOCAP_ATTN_H
+#define MOCAP_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOCAP_OK = 0,
+  MOCAP_ERR_INVALID_ARG = 1, /* a malformed argument: nothing enqueued          */
+  MOCAP_ERR_UNSUPPORTED = 2, /* well formed, but outside what the kernels do   */
+  MOCAP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required     */
+  MOCAP_ERR_HIP = 4          /* the HIP runtime reported an error              */
+} mocap_status;
+
+/*
+ * A block-addressed KV store (host struct describing caller-owned device
+ * memory).  Each physical block holds block_size consecutive positions of
+ * all h_kv heads.
+ *   k_pool : bf16 [num_blocks][h_kv][block_size][head_dim]   row per position
+ *   v_pool : bf16 [num_blocks][h_kv][head_dim][block_size]   transposed inside
+ *            each block, so one head-dim coordinate of consecutive positions
+ *            is contiguous (the layout the P*V product consumes).
+ * block_size must be a positive multiple of 64; head_dim is 64 or 128.
+ */
+typedef struct {
+  void* k_pool;
+  void* v_pool;
+  int32_t num_blocks;
+  int32_t block_size;
+  int32_t h_kv;
+  int32_t head_dim;
+} mocap_kv_store;
+
+/*
+ * mocap_kv_append -- store one chunk's newly produced keys/values
+ * (Section 2.2: the KV of earlier chunks stays live for later chunks;
+ * Section 4.1: each stage first produces the chunk's new KV cache).
+ *
+ *   kv          store to write into (see mocap_kv_store)
+ *   block_table device int32 [n_table], logical block -> physical block
+ *   start_pos   P_c, absolute position of the chunk's first token (>= 0)
+ *   chunk_len   L_c (>= 0); 0 is a no-op
+ *   k_chunk     device bf16 [chunk_len][h_kv][head_dim]
+ *   v_chunk     device bf16 [chunk_len][h_kv][head_dim]
+ *   stream      hipStream_t or NULL
+ *
+ * Positions start_pos .. start_pos + chunk_len - 1 are written bit for bit;
+ * nothing else in the pools changes.  Requires
+ * ceil((start_pos + chunk_len) / block_size) <= n_table.
+ * Errors: INVALID_ARG for null/misaligned pointers, negative sizes or a table
+ * that is too short; UNSUPPORTED for head_dim or block_size outside the above;
+ * HIP if the launch fails.
+ */
+mocap_status mocap_kv_append(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                             int64_t start_pos, int32_t chunk_len, const void* k_chunk,
+                             const void* v_chunk, void* stream);
+
+/*
+ * mocap_chunk_attn_workspace_size -- plan the KV split of one chunk and size
+ * its workspace.
+ *
+ * The keys a chunk sees may be cut into ranges that are processed in
+ * parallel and then combined by their log-sum-exp (the same combination a
+ * debtor stage needs when it reads part of its KV remotely and part locally,
+ * Section 4.1).  num_splits is the number of ranges: 1 = unsplit (no
+ * workspace), n >= 2 = the prefix [0, P_c) cut into n - 1 ranges on 64-key
+ * tile boundaries plus the chunk's own keys as the last range, 0 = let the
+ * library choose from the shape and the current device's compute-unit count.
+ * A requested count is clamped to what the prefix allows (1 when P_c = 0).
+ *
+ *   splits_out  (may be NULL) the number of ranges that will be used
+ *   bytes_out   workspace bytes mocap_chunk_attn needs for this plan (0 when
+ *               the plan is unsplit)
+ * Errors: INVALID_ARG for a null bytes_out or malformed sizes; UNSUPPORTED
+ * for head_dim not in {64, 128}; HIP if the device query fails (auto only).
+ */
+mocap_status mocap_chunk_attn_workspace_size(int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                             int32_t h_kv, int32_t head_dim, int32_t num_splits,
+                                             int32_t* splits_out, size_t* bytes_out);
+
+/*
+ * mocap_chunk_attn -- causal attention of one chunk over its prefix and itself
+ * (Section 2.2; cost c_i (p_i + c_i) by Eq. (1)).
+ *
+ *   kv, block_table, n_table  KV store holding positions [0, prefix_len +
+ *               chunk_len): the chunk's own KV must already be appended, on
+ *               this stream or otherwise ordered before this call
+ *   q           device bf16 [chunk_len][h_q][head_dim]
+ *   prefix_len  P_c (>= 0);  chunk_len  L_c (>= 0, 0 is a no-op)
+ *   h_q, h_kv   query / KV head counts, h_q a multiple of h_kv, h_kv equal to
+ *               kv->h_kv; head_dim equal to kv->head_dim
+ *   scale       score scale, finite and > 0 (typically 1/sqrt(head_dim))
+ *   o           device bf16 [chunk_len][h_q][head_dim]           (output)
+ *   lse         device fp32 [h_q][chunk_len], natural log          (output)
+ *   workspace   device scratch of workspace_bytes, or NULL when the plan is
+ *               unsplit; its contents on entry do not matter
+ *   num_splits  as in mocap_chunk_attn_workspace_size
+ *   stream      hipStream_t or NULL
+ *
+ * The same (shape, num_splits, device) always gives the same plan and the
+ * same bits, whatever physical blocks the table names.
+ * Errors: INVALID_ARG for null/misaligned pointers, negative sizes, h_q not a
+ * multiple of h_kv, head counts or head_dim that differ from the store, a
+ * non-positive or non-finite scale, or a table shorter than
+ * ceil((prefix_len + chunk_len) / block_size); UNSUPPORTED for head_dim not in
+ * {64, 128} or block_size not a positive multiple of 64; WORKSPACE when the
+ * plan needs more than workspace_bytes; HIP if a launch fails.
+ */
+mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                              const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                              int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                              void* workspace, size_t workspace_bytes, int32_t num_splits,
+                              void* stream);
+
+/*
+ * mocap_chunk_plan -- chunk lengths for a prompt of seq_len tokens (host only,
+ * no device work).
+ *
+ *   balanced = 0: uniform; boundary c at floor(c * seq_len / num_chunks).
+ *   balanced = 1: every chunk gets the same causal attention work
+ *     L_c (P_c + L_c / 2), the balancing goal behind Section 4.2's
+ *     latency-balanced partitioning applied to the attention term of Eq. (1).
+ *     Cumulative work up to boundary x is x^2 / 2, so boundary c sits at
+ *     seq_len * sqrt(c / num_chunks), rounded to the nearest multiple of
+ *     align (exact integer arithmetic).  seq_len must be a multiple of align.
+ *   lengths_out host int32 [num_chunks]
+ * Errors: INVALID_ARG for non-positive sizes, a null output, seq_len not a
+ * multiple of align (balanced), an exact rounding tie, an empty chunk, or a
+ * length that does not fit in int32.
+ */
+mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align, int32_t balanced,
+                              int32_t* lengths_out);
+
+/* A static, human-readable name for a status code. */
+const char* mocap_status_string(mocap_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOCAP_ATTN_H */

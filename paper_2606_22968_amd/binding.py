@@ -1,0 +1,191 @@
+"""ctypes binding of libmocap_attn (argument marshalling only).
+
+Each function carries the name of the C entry point it wraps and does no
+arithmetic of its own: it checks tensor dtypes, devices, shapes and
+contiguity, passes raw pointers, and turns a non-zero status into
+``MocapError``.  The library must have been built (``build.py``); if it is
+missing this module raises instead of falling back to anything else.
+"""
+import ctypes
+import os
+from typing import List, Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmocap_attn.so")
+
+MOCAP_OK = 0
+MOCAP_ERR_INVALID_ARG = 1
+MOCAP_ERR_UNSUPPORTED = 2
+MOCAP_ERR_WORKSPACE = 3
+MOCAP_ERR_HIP = 4
+
+# Every entry point the header declares.
+EXPORTED = (
+    "mocap_kv_append",
+    "mocap_chunk_attn_workspace_size",
+    "mocap_chunk_attn",
+    "mocap_chunk_plan",
+    "mocap_status_string",
+)
+
+
+class MocapError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {mocap_status_string(status)} ({status})")
+
+
+class mocap_kv_store(ctypes.Structure):
+    _fields_ = [
+        ("k_pool", ctypes.c_void_p),
+        ("v_pool", ctypes.c_void_p),
+        ("num_blocks", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("h_kv", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load_library():
+    """Load libmocap_attn.so from the package directory (no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2606_22968_amd.build` "
+            "(or __graft_entry__.build()) before using the HIP path")
+    lib = ctypes.CDLL(LIB_PATH)
+    st = ctypes.c_int
+    lib.mocap_status_string.restype = ctypes.c_char_p
+    lib.mocap_status_string.argtypes = [st]
+    lib.mocap_kv_append.restype = st
+    lib.mocap_kv_append.argtypes = [
+        ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.mocap_chunk_attn_workspace_size.restype = st
+    lib.mocap_chunk_attn_workspace_size.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
+    lib.mocap_chunk_attn.restype = st
+    lib.mocap_chunk_attn.argtypes = [
+        ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+        ctypes.c_int32, ctypes.c_void_p]
+    lib.mocap_chunk_plan.restype = st
+    lib.mocap_chunk_plan.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.POINTER(ctypes.c_int32)]
+    _lib = lib
+    return lib
+
+
+def mocap_status_string(status: int) -> str:
+    return load_library().mocap_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != MOCAP_OK:
+        raise MocapError(status, where)
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _require(t: torch.Tensor, dtype, name: str, ndim: Optional[int] = None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {tuple(t.shape)}")
+
+
+class KvStore:
+    """Caller-owned block pools (torch device memory) plus the C descriptor.
+
+    k_pool: bf16 [num_blocks][h_kv][block_size][head_dim]
+    v_pool: bf16 [num_blocks][h_kv][head_dim][block_size]
+    """
+
+    def __init__(self, num_blocks: int, block_size: int, h_kv: int, head_dim: int,
+                 device="cuda", fill: Optional[float] = None):
+        self.num_blocks, self.block_size, self.h_kv, self.head_dim = num_blocks, block_size, h_kv, head_dim
+        self.k_pool = torch.empty((num_blocks, h_kv, block_size, head_dim), dtype=torch.bfloat16, device=device)
+        self.v_pool = torch.empty((num_blocks, h_kv, head_dim, block_size), dtype=torch.bfloat16, device=device)
+        if fill is not None:
+            self.k_pool.fill_(fill)
+            self.v_pool.fill_(fill)
+
+    def descriptor(self) -> mocap_kv_store:
+        return mocap_kv_store(self.k_pool.data_ptr(), self.v_pool.data_ptr(), self.num_blocks,
+                              self.block_size, self.h_kv, self.head_dim)
+
+
+def mocap_kv_append(store: KvStore, block_table: torch.Tensor, start_pos: int,
+                    k_chunk: torch.Tensor, v_chunk: torch.Tensor, stream=None) -> None:
+    _require(block_table, torch.int32, "block_table", 1)
+    _require(k_chunk, torch.bfloat16, "k_chunk", 3)
+    _require(v_chunk, torch.bfloat16, "v_chunk", 3)
+    if k_chunk.shape != v_chunk.shape or tuple(k_chunk.shape[1:]) != (store.h_kv, store.head_dim):
+        raise ValueError("k_chunk/v_chunk must be [chunk_len][h_kv][head_dim] of the store")
+    desc = store.descriptor()
+    _check(load_library().mocap_kv_append(
+        ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), int(start_pos),
+        k_chunk.shape[0], k_chunk.data_ptr(), v_chunk.data_ptr(), _stream_handle(stream)),
+        "mocap_kv_append")
+
+
+def mocap_chunk_attn_workspace_size(prefix_len: int, chunk_len: int, h_q: int, h_kv: int,
+                                    head_dim: int, num_splits: int = 0) -> Tuple[int, int]:
+    """Returns (number of KV ranges, workspace bytes)."""
+    splits = ctypes.c_int32(0)
+    nbytes = ctypes.c_size_t(0)
+    _check(load_library().mocap_chunk_attn_workspace_size(
+        int(prefix_len), int(chunk_len), int(h_q), int(h_kv), int(head_dim), int(num_splits),
+        ctypes.byref(splits), ctypes.byref(nbytes)), "mocap_chunk_attn_workspace_size")
+    return splits.value, nbytes.value
+
+
+def mocap_chunk_attn(store: KvStore, block_table: torch.Tensor, q: torch.Tensor, prefix_len: int,
+                     scale: float, o: torch.Tensor, lse: torch.Tensor,
+                     workspace: Optional[torch.Tensor] = None, num_splits: int = 0,
+                     stream=None) -> None:
+    """q, o: bf16 [chunk_len][h_q][head_dim]; lse: fp32 [h_q][chunk_len]."""
+    _require(block_table, torch.int32, "block_table", 1)
+    _require(q, torch.bfloat16, "q", 3)
+    _require(o, torch.bfloat16, "o", 3)
+    _require(lse, torch.float32, "lse", 2)
+    chunk_len, h_q, head_dim = q.shape
+    if o.shape != q.shape or tuple(lse.shape) != (h_q, chunk_len):
+        raise ValueError("o must match q and lse must be [h_q][chunk_len]")
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _require(workspace, workspace.dtype, "workspace")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    desc = store.descriptor()
+    _check(load_library().mocap_chunk_attn(
+        ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), q.data_ptr(),
+        int(prefix_len), chunk_len, h_q, store.h_kv, head_dim, float(scale), o.data_ptr(),
+        lse.data_ptr(), ws_ptr, ws_bytes, int(num_splits), _stream_handle(stream)),
+        "mocap_chunk_attn")
+
+
+def mocap_chunk_plan(seq_len: int, num_chunks: int, align: int = 128, balanced: bool = False) -> List[int]:
+    out = (ctypes.c_int32 * num_chunks)()
+    _check(load_library().mocap_chunk_plan(int(seq_len), int(num_chunks), int(align), int(bool(balanced)), out),
+           "mocap_chunk_plan")
+    return list(out)

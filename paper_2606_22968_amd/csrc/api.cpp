@@ -1,0 +1,293 @@
+// Host side of libmocap_attn: argument validation, chunk and split planning,
+// and kernel dispatch.  Every check runs before anything is enqueued.
+#include "mocap_attn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+
+#include "internal.h"
+
+namespace {
+
+using mocap::kTileKeys;
+using mocap::kWaveRows;
+using mocap::kWavesPerGroup;
+
+constexpr int kMaxDevices = 64;
+constexpr int64_t kMaxPositions = ((int64_t)1 << 31) - 128;
+std::atomic<int> g_cu_count[kMaxDevices];  // 0 = not yet queried
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+bool supported_head_dim(int d) { return d == 64 || d == 128; }
+
+mocap_status device_cu_count(int* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOCAP_ERR_HIP;
+  if (dev >= 0 && dev < kMaxDevices) {
+    const int cached = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (cached > 0) {
+      *out = cached;
+      return MOCAP_OK;
+    }
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return MOCAP_ERR_HIP;
+  if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(cus, std::memory_order_relaxed);
+  *out = cus;
+  return MOCAP_OK;
+}
+
+// Query heads per workgroup: the largest of 4, 2, 1 dividing the GQA group.
+int heads_per_wg(int group) { return group % 4 == 0 ? 4 : (group % 2 == 0 ? 2 : 1); }
+
+struct Plan {
+  int hp;
+  int row_groups;
+  int base_wgs;      // workgroups of one KV range
+  int64_t prefix_tiles;
+  int n_ranges;
+  size_t ws_bytes;
+};
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+size_t workspace_for(int n_ranges, int64_t chunk_len, int h_q, int head_dim) {
+  if (n_ranges <= 1) return 0;
+  const size_t rows = (size_t)n_ranges * (size_t)h_q * (size_t)chunk_len;
+  return round_up(rows * (size_t)head_dim * sizeof(float), 256) + round_up(rows * sizeof(float), 256);
+}
+
+// Number of KV ranges to use.  Auto mode cuts the prefix until the launch has
+// roughly two workgroups per compute unit, keeping every prefix range at
+// least 8 tiles (512 keys) long.
+int choose_ranges(int64_t prefix_tiles, int base_wgs, int requested, int cu_count) {
+  if (prefix_tiles <= 0) return 1;
+  if (requested >= 1) {
+    if (requested == 1) return 1;
+    const int64_t parts = requested - 1 < prefix_tiles ? requested - 1 : prefix_tiles;
+    return (int)parts + 1;
+  }
+  if (base_wgs >= cu_count) return 1;
+  int64_t parts = (2 * (int64_t)cu_count + base_wgs - 1) / base_wgs - 1;
+  const int64_t max_parts = prefix_tiles / 8;
+  if (parts > max_parts) parts = max_parts;
+  if (parts < 1) return 1;
+  if (parts > 64) parts = 64;
+  return (int)parts + 1;
+}
+
+mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
+                       int32_t head_dim, int32_t num_splits, Plan* plan) {
+  const int group = h_q / h_kv;
+  plan->hp = heads_per_wg(group);
+  const int rows_per_wg = kWaveRows * (kWavesPerGroup / plan->hp);
+  plan->row_groups = (int)((chunk_len + rows_per_wg - 1) / rows_per_wg);
+  const int64_t base = (int64_t)(h_q / plan->hp) * plan->row_groups;
+  if (base > (int64_t)1 << 24) return MOCAP_ERR_UNSUPPORTED;
+  plan->base_wgs = (int)base;
+  plan->prefix_tiles = (prefix_len + kTileKeys - 1) / kTileKeys;
+  int cus = 0;
+  if (num_splits == 0 && plan->prefix_tiles > 0) {
+    const mocap_status st = device_cu_count(&cus);
+    if (st != MOCAP_OK) return st;
+  }
+  plan->n_ranges = choose_ranges(plan->prefix_tiles, plan->base_wgs, num_splits, cus);
+  plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
+  return MOCAP_OK;
+}
+
+mocap_status check_store(const mocap_kv_store* kv) {
+  if (kv == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (kv->num_blocks <= 0 || kv->block_size <= 0 || kv->h_kv <= 0 || kv->head_dim <= 0)
+    return MOCAP_ERR_INVALID_ARG;
+  if (!supported_head_dim(kv->head_dim)) return MOCAP_ERR_UNSUPPORTED;
+  if (kv->block_size % kTileKeys != 0) return MOCAP_ERR_UNSUPPORTED;
+  return MOCAP_OK;
+}
+
+mocap_status check_positions(const mocap_kv_store* kv, int32_t n_table, int64_t start, int32_t len) {
+  if (start < 0 || len < 0 || n_table < 0) return MOCAP_ERR_INVALID_ARG;
+  // Kernels index positions with 32-bit integers.
+  if (start + (int64_t)len > kMaxPositions) return MOCAP_ERR_INVALID_ARG;
+  const int64_t end = start + len;
+  const int64_t blocks_needed = (end + kv->block_size - 1) / kv->block_size;
+  if (blocks_needed > n_table) return MOCAP_ERR_INVALID_ARG;
+  return MOCAP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mocap_status_string(mocap_status status) {
+  switch (status) {
+    case MOCAP_OK: return "MOCAP_OK";
+    case MOCAP_ERR_INVALID_ARG: return "MOCAP_ERR_INVALID_ARG";
+    case MOCAP_ERR_UNSUPPORTED: return "MOCAP_ERR_UNSUPPORTED";
+    case MOCAP_ERR_WORKSPACE: return "MOCAP_ERR_WORKSPACE";
+    case MOCAP_ERR_HIP: return "MOCAP_ERR_HIP";
+  }
+  return "MOCAP_ERR_UNKNOWN";
+}
+
+mocap_status mocap_kv_append(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                             int64_t start_pos, int32_t chunk_len, const void* k_chunk,
+                             const void* v_chunk, void* stream) {
+  mocap_status st = check_store(kv);
+  if (st != MOCAP_OK) return st;
+  st = check_positions(kv, n_table, start_pos, chunk_len);
+  if (st != MOCAP_OK) return st;
+  if (chunk_len == 0) return MOCAP_OK;
+  if (!kv->k_pool || !kv->v_pool || !block_table || !k_chunk || !v_chunk) return MOCAP_ERR_INVALID_ARG;
+  if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || !aligned16(block_table) ||
+      !aligned16(k_chunk) || !aligned16(v_chunk))
+    return MOCAP_ERR_INVALID_ARG;
+
+  mocap::AppendLaunch p;
+  p.k_chunk = static_cast<const uint16_t*>(k_chunk);
+  p.v_chunk = static_cast<const uint16_t*>(v_chunk);
+  p.k_pool = static_cast<uint16_t*>(kv->k_pool);
+  p.v_pool = static_cast<uint16_t*>(kv->v_pool);
+  p.table = block_table;
+  p.start_pos = start_pos;
+  p.chunk_len = chunk_len;
+  p.h_kv = kv->h_kv;
+  p.block_size = kv->block_size;
+  if (mocap::launch_kv_append(p, kv->head_dim, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return MOCAP_ERR_HIP;
+  return MOCAP_OK;
+}
+
+mocap_status mocap_chunk_attn_workspace_size(int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                             int32_t h_kv, int32_t head_dim, int32_t num_splits,
+                                             int32_t* splits_out, size_t* bytes_out) {
+  if (bytes_out == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (prefix_len < 0 || chunk_len < 0 || h_q <= 0 || h_kv <= 0 || h_q % h_kv != 0 || num_splits < 0)
+    return MOCAP_ERR_INVALID_ARG;
+  if (prefix_len + (int64_t)chunk_len > kMaxPositions) return MOCAP_ERR_INVALID_ARG;
+  if (!supported_head_dim(head_dim)) return MOCAP_ERR_UNSUPPORTED;
+  if (chunk_len == 0) {
+    if (splits_out) *splits_out = 1;
+    *bytes_out = 0;
+    return MOCAP_OK;
+  }
+  Plan plan;
+  const mocap_status st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
+  if (st != MOCAP_OK) return st;
+  if (splits_out) *splits_out = plan.n_ranges;
+  *bytes_out = plan.ws_bytes;
+  return MOCAP_OK;
+}
+
+mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                              const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                              int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                              void* workspace, size_t workspace_bytes, int32_t num_splits,
+                              void* stream) {
+  mocap_status st = check_store(kv);
+  if (st != MOCAP_OK) return st;
+  if (h_q <= 0 || h_kv <= 0 || h_q % h_kv != 0 || h_kv != kv->h_kv || head_dim != kv->head_dim)
+    return MOCAP_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return MOCAP_ERR_INVALID_ARG;
+  if (num_splits < 0) return MOCAP_ERR_INVALID_ARG;
+  st = check_positions(kv, n_table, prefix_len, chunk_len);
+  if (st != MOCAP_OK) return st;
+  if (chunk_len == 0) return MOCAP_OK;
+  if (!kv->k_pool || !kv->v_pool || !block_table || !q || !o || !lse) return MOCAP_ERR_INVALID_ARG;
+  if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || !aligned16(block_table) || !aligned16(q) ||
+      !aligned16(o) || !aligned16(lse))
+    return MOCAP_ERR_INVALID_ARG;
+
+  Plan plan;
+  st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
+  if (st != MOCAP_OK) return st;
+  const int64_t total = (int64_t)plan.base_wgs * plan.n_ranges;
+  if (total > 0x7fffffff) return MOCAP_ERR_UNSUPPORTED;
+  if (plan.n_ranges > 1) {
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < plan.ws_bytes)
+      return MOCAP_ERR_WORKSPACE;
+  }
+
+  mocap::AttnLaunch p;
+  p.q = static_cast<const uint16_t*>(q);
+  p.k_pool = static_cast<const uint16_t*>(kv->k_pool);
+  p.v_pool = static_cast<const uint16_t*>(kv->v_pool);
+  p.table = block_table;
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.prefix_len = (int32_t)prefix_len;
+  p.prefix_tiles = (int32_t)plan.prefix_tiles;
+  p.chunk_len = chunk_len;
+  p.h_q = h_q;
+  p.h_kv = h_kv;
+  p.group = h_q / h_kv;
+  p.heads_per_wg = plan.hp;
+  p.row_groups = plan.row_groups;
+  p.block_size = kv->block_size;
+  p.n_ranges = plan.n_ranges;
+  p.total_wgs = (int)total;
+  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  p.ws_o = nullptr;
+  p.ws_lse = nullptr;
+  if (plan.n_ranges > 1) {
+    const size_t rows = (size_t)plan.n_ranges * (size_t)h_q * (size_t)chunk_len;
+    p.ws_o = static_cast<float*>(workspace);
+    p.ws_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                        round_up(rows * (size_t)head_dim * sizeof(float), 256));
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (mocap::launch_chunk_attn(p, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
+  if (plan.n_ranges > 1) {
+    mocap::MergeLaunch m;
+    m.ws_o = p.ws_o;
+    m.ws_lse = p.ws_lse;
+    m.o = p.o;
+    m.lse = lse;
+    m.chunk_len = chunk_len;
+    m.h_q = h_q;
+    m.n_ranges = plan.n_ranges;
+    if (mocap::launch_lse_merge(m, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
+  }
+  return MOCAP_OK;
+}
+
+mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align, int32_t balanced,
+                              int32_t* lengths_out) {
+  if (seq_len <= 0 || num_chunks <= 0 || lengths_out == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (seq_len > ((int64_t)1 << 40)) return MOCAP_ERR_INVALID_ARG;
+  typedef __int128 i128;
+  int64_t prev = 0;
+  for (int c = 1; c <= num_chunks; ++c) {
+    int64_t bound;
+    if (c == num_chunks) {
+      bound = seq_len;
+    } else if (!balanced) {
+      bound = (int64_t)((i128)c * seq_len / num_chunks);
+    } else {
+      if (align <= 0 || seq_len % align != 0) return MOCAP_ERR_INVALID_ARG;
+      // Boundary in units of `align`: u = A sqrt(c / M) with A = seq_len / align.
+      // The nearest integer k satisfies M (2k - 1)^2 <= 4 A^2 c < M (2k + 1)^2.
+      const i128 A = seq_len / align;
+      const i128 rhs = 4 * A * A * (i128)c;
+      int64_t k = (int64_t)std::floor((double)A * std::sqrt((double)c / num_chunks) + 0.5);
+      auto lower_ok = [&](int64_t kk) { return kk <= 0 || (i128)num_chunks * (2 * (i128)kk - 1) * (2 * (i128)kk - 1) <= rhs; };
+      while (!lower_ok(k)) --k;
+      while (lower_ok(k + 1)) ++k;
+      const i128 edge = (i128)num_chunks * (2 * (i128)k - 1) * (2 * (i128)k - 1);
+      if (k > 0 && edge == rhs) return MOCAP_ERR_INVALID_ARG;  // exact tie
+      bound = k * (int64_t)align;
+    }
+    const int64_t len = bound - prev;
+    if (len <= 0 || len > 0x7fffffff) return MOCAP_ERR_INVALID_ARG;
+    lengths_out[c - 1] = (int32_t)len;
+    prev = bound;
+  }
+  return MOCAP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+// Internal launch descriptions shared by the host API and the HIP kernels of
+// libmocap_attn.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mocap {
+
+constexpr int kTileKeys = 64;          // keys per KV tile (LDS stage)
+constexpr int kWaveRows = 64;          // query rows owned by one wavefront
+constexpr int kWavesPerGroup = 4;      // wavefronts per workgroup
+constexpr int kGroupThreads = 64 * kWavesPerGroup;
+
+// One launch of the attention kernel: every workgroup owns `heads_per_wg`
+// query heads of one GQA group times `64 * 4 / heads_per_wg` query rows, for
+// one KV range.
+struct AttnLaunch {
+  const uint16_t* q;        // bf16 [L][Hq][D]
+  const uint16_t* k_pool;   // bf16 [nb][Hkv][bs][D]
+  const uint16_t* v_pool;   // bf16 [nb][Hkv][D][bs]
+  const int32_t* table;     // logical block -> physical block
+  uint16_t* o;              // bf16 [L][Hq][D]         (unsplit)
+  float* lse;               // fp32 [Hq][L]            (unsplit)
+  float* ws_o;              // fp32 [R][Hq][L][D]      (split partials)
+  float* ws_lse;            // fp32 [R][Hq][L]
+  int32_t prefix_len;       // P (P + L < 2^31 - 128, checked on the host)
+  int32_t prefix_tiles;     // ceil(P / 64)
+  int32_t chunk_len;        // L
+  int32_t h_q;
+  int32_t h_kv;
+  int32_t group;            // Hq / Hkv
+  int32_t heads_per_wg;     // 4, 2 or 1 (divides group)
+  int32_t row_groups;       // ceil(L / rows_per_wg)
+  int32_t block_size;
+  int32_t n_ranges;         // 1 = unsplit; else prefix ranges + 1 chunk range
+  int32_t total_wgs;
+  float scale_log2;         // scale * log2(e)
+};
+
+struct AppendLaunch {
+  const uint16_t* k_chunk;  // bf16 [L][Hkv][D]
+  const uint16_t* v_chunk;  // bf16 [L][Hkv][D]
+  uint16_t* k_pool;
+  uint16_t* v_pool;
+  const int32_t* table;
+  int64_t start_pos;
+  int32_t chunk_len;
+  int32_t h_kv;
+  int32_t block_size;
+};
+
+struct MergeLaunch {
+  const float* ws_o;        // fp32 [R][Hq][L][D]
+  const float* ws_lse;      // fp32 [R][Hq][L]
+  uint16_t* o;              // bf16 [L][Hq][D]
+  float* lse;               // fp32 [Hq][L]
+  int32_t chunk_len;
+  int32_t h_q;
+  int32_t n_ranges;
+};
+
+hipError_t launch_chunk_attn(const AttnLaunch& p, int head_dim, hipStream_t stream);
+hipError_t launch_kv_append(const AppendLaunch& p, int head_dim, hipStream_t stream);
+hipError_t launch_lse_merge(const MergeLaunch& p, int head_dim, hipStream_t stream);
+
+}  // namespace mocap

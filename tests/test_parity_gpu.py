@@ -1,0 +1,74 @@
+"""GPU parity: the HIP path against the fp64 oracle on the same seeded bf16
+inputs.  Small shapes are compared on every output; the full-size workloads
+on a seeded sample of rows (every chunk x every head x 8 rows), in the launch
+configuration the benchmark times (automatic split planning)."""
+import pytest
+import torch
+
+from helpers import check_chunks, run_gpu, say, workload_inputs
+from paper_2606_22968_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def test_small_d64_workload_all_rows(gpu, oracle_lib):
+    w = synth.WORKLOADS["small_d64"]
+    say(f"[case] {w.name}")
+    q, k, v = workload_inputs(w.seed, w.seq_len, w.h_q, w.h_kv, w.head_dim)
+    lengths = binding.mocap_chunk_plan(w.seq_len, w.num_chunks, 1, balanced=False)
+    runner = run_gpu(q, k, v, lengths, w.scale, block_size=w.block_size)
+    check_chunks(oracle_lib, runner, q, k, v, w.scale, label=w.name)
+
+
+@pytest.mark.parametrize("h_q,h_kv,d,lengths", [
+    (32, 8, 128, [512, 512, 512, 512]),      # Llama-3-8B heads, short sequence
+    (64, 8, 128, [256, 256, 256, 256]),      # Llama-3-70B heads, short sequence
+])
+def test_reduced_model_shapes_all_rows(gpu, oracle_lib, h_q, h_kv, d, lengths):
+    say(f"[case] reduced h_q={h_q} h_kv={h_kv} d={d} lengths={lengths}")
+    q, k, v = synth.make_qkv(20 + h_q, sum(lengths), h_q, h_kv, d)
+    scale = d ** -0.5
+    runner = run_gpu(q, k, v, lengths, scale)
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"reduced {h_q}/{h_kv}/{d}")
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", [(8, 8, 64), (8, 4, 128), (8, 2, 128), (16, 2, 64), (12, 4, 128)])
+def test_ragged_chunks_all_rows(gpu, oracle_lib, h_q, h_kv, d):
+    # Chunk and prefix lengths that are not multiples of the 64-key tile, a
+    # store of 64-position blocks, and NaN in every unwritten pool slot.
+    lengths = [1, 7, 100, 129, 13, 255, 64, 3]
+    say(f"[case] ragged h_q={h_q} h_kv={h_kv} d={d}")
+    q, k, v = synth.make_qkv(30 + h_q + d, sum(lengths), h_q, h_kv, d)
+    scale = 0.11
+    runner = run_gpu(q, k, v, lengths, scale, block_size=64, pool_fill=float("nan"))
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"ragged {h_q}/{h_kv}/{d}")
+
+
+@pytest.mark.parametrize("splits", [1, 2, 3, 7, 0])
+def test_forced_splits(gpu, oracle_lib, splits):
+    lengths = [1500, 37, 600, 1]
+    say(f"[case] forced splits={splits}")
+    q, k, v = synth.make_qkv(40, sum(lengths), 16, 4, 128)
+    scale = 128 ** -0.5
+    runner = run_gpu(q, k, v, lengths, scale, block_size=128, num_splits=splits)
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"splits={splits} plan={runner.splits}")
+
+
+def _workload_plan(w):
+    return binding.mocap_chunk_plan(w.seq_len, w.num_chunks, w.align, balanced=(w.chunking == "balanced"))
+
+
+@pytest.mark.parametrize("name", ["llama8b_32k_uniform", "llama8b_128k_balanced", "llama70b_64k_uniform",
+                                  "llama8b_128k_paged"])
+def test_full_size_workload_sampled_rows(gpu, oracle_lib, name):
+    w = synth.WORKLOADS[name]
+    say(f"[case] {name}: generating inputs")
+    q, k, v = workload_inputs(w.seed, w.seq_len, w.h_q, w.h_kv, w.head_dim)
+    lengths = _workload_plan(w)
+    n_blocks = w.seq_len // w.block_size
+    table = synth.permuted_table(n_blocks, w.perm_seed) if w.permuted else None
+    say(f"[case] {name}: GPU run, {len(lengths)} chunks")
+    runner = run_gpu(q, k, v, lengths, w.scale, block_size=w.block_size, table=table)
+    say(f"[case] {name}: splits per chunk {runner.splits}")
+    check_chunks(oracle_lib, runner, q, k, v, w.scale,
+                 rows_of=lambda c, n: synth.sample_rows(n, 1000 * w.seed + c), label=name)
