@@ -21,14 +21,17 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in VGPRs: the score accumulators feed the softmax VALU work
+    # directly, and only read-only operands are left for the AGPRs.
+    "-mllvm", "-amdgpu-mfma-vgpr-form=true",
     "-Wno-unused-command-line-argument",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, verbose: bool, build_dir: str, extra_flags) -> str:
+    obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC, *FLAGS, *extra_flags, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -38,17 +41,32 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, extra_flags=(), lib_path: str = LIB, build_dir: str = BUILD_DIR) -> str:
+    """Compile every source and link ``lib_path``.  ``extra_flags`` (e.g. -D
+    tuning macros) and an alternative output location serve experiments."""
+    os.makedirs(build_dir, exist_ok=True)
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, verbose, build_dir, tuple(extra_flags)), SOURCES))
+    tmp = lib_path + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    _check_stubs(tmp)
+    os.replace(tmp, lib_path)
+    return lib_path
+
+
+def _check_stubs(lib: str) -> None:
+    """Fail if a kernel's host launch stub was not emitted.
+
+    If a kernel body does not compile for the host pass, clang can drop the
+    template's stub without an error, leaving an undefined symbol that only
+    shows up when the library is loaded."""
+    out = subprocess.run(["nm", "-C", lib], check=True, capture_output=True, text=True).stdout
+    missing = [ln.strip() for ln in out.splitlines() if " U " in ln and "__device_stub__" in ln]
+    if missing:
+        raise RuntimeError("kernel launch stubs missing from " + lib + ":\n" + "\n".join(missing))
 
 
 if __name__ == "__main__":

@@ -91,17 +91,20 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
   return w;
 }
 
-// Rows keep a running maximum m (base-2 units) that only moves when a block's
-// maximum exceeds it by more than kRescaleSlack; between moves the
-// probabilities exp2(s - m) stay below 2^kRescaleSlack, which fp32 sums and
-// bf16 probabilities hold without loss of relative precision.  The final
-// normalisation uses the same m for numerator and denominator, so the result
-// does not depend on when m moved.  The O accumulator is therefore rescaled
-// only on those rare moves, and a 64-key tile can be consumed as two
-// independent 32-key halves.
-constexpr float kRescaleSlack = 8.0f;
+// Softmax bookkeeping.  Each query row keeps a reference exponent m (base 2)
+// and accumulates p = exp2(s * scale * log2(e) - m) without first taking the
+// block maximum.  m is only a scale: the result sum(p v) / sum(p) does not
+// depend on it as long as nothing overflows.  A block whose partial row sum
+// exceeds 2^kSumLimit (or is not finite, e.g. the first block, where m is
+// still -inf) is recomputed on a slow path that moves m to the block's true
+// maximum and rescales the O accumulator and the running sum.  With
+// attention scores of ordinary size this happens for the first block of a
+// row and almost never again, so the fast path spends no VALU work on maxima
+// and the O accumulator is almost never touched outside the MFMAs.
+constexpr float kSumLimit = 1048576.0f;  // 2^20
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
 
 // LDS layout of one stage (no padding; 16-byte chunks XOR-swizzled so the
 // MFMA operand reads of 8 consecutive lanes hit 8 different 16-byte bank
@@ -112,8 +115,29 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // 8 lanes; k_swizzle separates r from r + 8.
 __device__ __forceinline__ int k_swizzle(int r) { return (r & 7) ^ ((r >> 1) & 4); }
 
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int N>
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v;
+  v[0] = (__bf16)a;
+  v[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
 template <int D>
 __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const AttnLaunch p) {
+  // Device pass only: the host pass needs just the launch stub, and these
+  // gfx950 builtins do not exist for the host target.
+#if defined(__HIP_DEVICE_COMPILE__)
   constexpr int KS = D / 16;                     // k-steps of the score product
   constexpr int MD = D / 32;                     // 32-wide blocks of the head dim
   constexpr int K_ROW_CHUNKS = D / 8;            // 16-byte chunks per K row
@@ -121,8 +145,9 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   constexpr int K_ELEMS = kTileKeys * D;
   constexpr int BUF_ELEMS = 2 * K_ELEMS;         // K tile + V^T tile
   constexpr int LOADS = K_ELEMS / 8 / kGroupThreads;  // 1 KiB wave loads per operand
+  constexpr int STAGES = 3;
 
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * BUF_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -136,7 +161,8 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int hp = p.heads_per_wg;
   const int blocks_per_wg = kWavesPerGroup / hp;
   const int head = item.head0 + (wave % hp);
-  const int row0 = (item.row_group * blocks_per_wg + wave / hp) * kWaveRows;
+  const int wg_row0 = item.row_group * blocks_per_wg * kWaveRows;
+  const int row0 = wg_row0 + (wave / hp) * kWaveRows;
   const int wg_row_end = min(L, (item.row_group + 1) * blocks_per_wg * kWaveRows);
 
   // Key range [lo, hi) of this launch item.
@@ -156,12 +182,14 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int tile_begin = lo / kTileKeys;
   const int tile_end = (wg_hi + kTileKeys - 1) / kTileKeys;
   const int valid_end = P + L;
+  // Tiles [fast_begin, fast_end) are visible to every row of the workgroup
+  // and need no mask; the others go through the masked path.
+  const int fast_begin = tile_begin + ((lo % kTileKeys) != 0 ? 1 : 0);
+  const int fast_end = max(fast_begin, min(tile_end, min(hi, P + wg_row0 + 1) / kTileKeys));
 
-  // Rows of this wavefront.  Keys at or beyond my_key_hi are masked for all of
-  // them; keys in [lo, full_vis_hi) are visible to all of them.
+  // Rows of this wavefront; keys at or beyond my_key_hi are masked for all of them.
   const int my_rows = min(row0 + kWaveRows, L) - row0;
   const int my_key_hi = my_rows > 0 ? min(hi, P + row0 + my_rows) : INT32_MIN;
-  const int full_vis_hi = min(hi, P + row0 + 1);
 
   // ---- Q fragments (B operand of S^T = K Q^T) ----
   bf16x8 qf[2][KS];
@@ -182,7 +210,8 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   // ---- tile staging: global -> LDS directly (global_load_lds_dwordx4) ----
   // Wave instruction j writes LDS chunks [(j*4 + wave)*64, +64) of an operand;
   // lane i fills chunk (j*4 + wave)*64 + i and fetches the global chunk that
-  // the swizzle maps there.
+  // the swizzle maps there.  Block-table entries are read with scalar loads.
+  const const_i32_ptr table = (const_i32_ptr)p.table;
   const int64_t head_stride = (int64_t)D * p.block_size;  // elements per (block, head)
   int k_src[LOADS], v_src[LOADS];  // per-lane element offsets inside a tile
 #pragma unroll
@@ -193,14 +222,14 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ (vr & 7);
     v_src[j] = vr * p.block_size + vc * 8;
   }
-  auto issue_tile = [&](int buf, int t) {
+  auto issue_tile = [&](int stage, int t) {
     const int pos0 = t * kTileKeys;
     const int lb = pos0 / p.block_size;
     const int slot0 = pos0 - lb * p.block_size;
-    const int64_t base = ((int64_t)p.table[lb] * p.h_kv + item.kv_head) * head_stride;
+    const int64_t base = ((int64_t)table[lb] * p.h_kv + item.kv_head) * head_stride;
     const uint16_t* kb = p.k_pool + base + (int64_t)slot0 * D;
     const uint16_t* vb = p.v_pool + base + slot0;
-    uint16_t* kl = lds + buf * BUF_ELEMS;
+    uint16_t* kl = lds + stage * BUF_ELEMS;
     uint16_t* vl = kl + K_ELEMS;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
@@ -221,102 +250,163 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const float sl2 = p.scale_log2;
   const int k_row_lo = key_row_order(l32);          // K row within a 32-key half
   const int v_row_sw = l32 & 7;                      // V^T swizzle of this lane's dim rows
+  const uint32_t ones = 0x3F803F80u;                 // bf16 pair (1, 1)
 
+  // Visibility of this lane's 16 keys of a 32-key half block, one bit per
+  // accumulator element i (key offset (i/8)*16 + half*8 + i%8 from `base`):
+  // keys in [lo, hi) and at or before the query's position.
+  auto visible_bits = [&](int base, int nb) -> uint32_t {
+    const int a = lo - base;
+    const int b = min(hi, P + row0 + nb * 32 + l32 + 1) - base;
+    // Offsets (i/8)*16 + i%8 increase with i, so the visible elements form
+    // one run [first_i(a), first_i(b)).
+    auto first_i = [](int x) { return x <= 0 ? 0 : x <= 8 ? x : x <= 16 ? 8 : x <= 24 ? x - 8 : 16; };
+    const int i0 = first_i(a), i1 = first_i(b);
+    return i1 > i0 ? (((1u << i1) - 1u) & ~((1u << i0) - 1u)) : 0u;
+  };
+
+  // One 32-key half of a tile: scores, softmax, P*V.
+  auto half_block = [&](const uint16_t* kl, const uint16_t* vl, int tstart, int sb, bool masked) {
+    f32x16 s[2];
+    s[0] = s[1] = f32x16{};
+    const int kr = sb * 32 + k_row_lo;
+    const uint16_t* krow = kl + kr * D;
+    const int ksw = k_swizzle(kr);
+    bf16x8 kf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      kf[ks] = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[0][ks], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[1][ks], s[1], 0, 0, 0);
+    }
+
+    // p = exp2(s * sl2 - m), packed to bf16 pairs in P*V B-operand order.
+    // Masked elements are cleared on the packed words (NaN-safe).
+    uint32_t pk[2][8];
+    uint32_t vis[2] = {0xFFFFu, 0xFFFFu};
+    if (masked) {
+      vis[0] = visible_bits(tstart + sb * 32 + half * 8, 0);
+      vis[1] = visible_bits(tstart + sb * 32 + half * 8, 1);
+    }
+    float rs[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const float neg_m = -m_run[nb];
+#pragma unroll
+      for (int i = 0; i < 16; i += 2) {
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m));
+        pk[nb][i / 2] = pack_bf16x2(e0, e1);
+      }
+    }
+    if (masked) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[nb], 2 * j, 1);
+          const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[nb], 2 * j + 1, 1);
+          pk[nb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
+        }
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[nb][j], ones, acc);
+      rs[nb] = acc;
+    }
+    const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
+    if (__builtin_amdgcn_ballot_w64(over) != 0) {
+      // Slow path: move m to the block maximum, rescale, recompute p.
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if ((vis[nb] >> i) & 1u) mx = fmaxf(mx, s[nb][i]);
+        mx = lane_pair_max(mx) * sl2;
+        const float m_new = fmaxf(m_run[nb], mx);
+        if (m_new != m_run[nb]) {
+          const float alpha = m_run[nb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
+          l_run[nb] *= alpha;
+#pragma unroll
+          for (int md = 0; md < MD; ++md) oacc[md][nb] *= alpha;
+          m_run[nb] = m_new;
+        }
+        const float neg_m = m_run[nb] == -INFINITY ? 0.f : -m_run[nb];
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+          const float e0 = ((vis[nb] >> i) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m)) : 0.f;
+          const float e1 = ((vis[nb] >> (i + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m)) : 0.f;
+          pk[nb][i / 2] = pack_bf16x2(e0, e1);
+          acc = dot2_bf16(pk[nb][i / 2], ones, acc);
+        }
+        rs[nb] = acc;
+      }
+    }
+    l_run[0] += rs[0];
+    l_run[1] += rs[1];
+
+    // O^T += V^T P^T over these 32 keys (2 k-steps of 16).
+    bf16x8 vf[2][MD];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int vchunk = ((sb * 2 + kk) * 2 + half) ^ v_row_sw;
+#pragma unroll
+      for (int md = 0; md < MD; ++md)
+        vf[kk][md] = *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 pb0 = __builtin_bit_cast(bf16x8, u32x4{pk[0][kk * 4], pk[0][kk * 4 + 1], pk[0][kk * 4 + 2], pk[0][kk * 4 + 3]});
+      const bf16x8 pb1 = __builtin_bit_cast(bf16x8, u32x4{pk[1][kk * 4], pk[1][kk * 4 + 1], pk[1][kk * 4 + 2], pk[1][kk * 4 + 3]});
+#pragma unroll
+      for (int md = 0; md < MD; ++md) {
+        oacc[md][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][md], pb0, oacc[md][0], 0, 0, 0);
+        oacc[md][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][md], pb1, oacc[md][1], 0, 0, 0);
+      }
+    }
+  };
+
+  // Prologue: the first two tiles in flight.
   if (tile_begin < tile_end) issue_tile(0, tile_begin);
+  if (tile_begin + 1 < tile_end) issue_tile(1, tile_begin + 1);
 
   for (int t = tile_begin; t < tile_end; ++t) {
-    const int buf = (t - tile_begin) & 1;
+    const int stage = (t - tile_begin) % STAGES;
     const int tstart = t * kTileKeys;
-    // Tile t has landed for this thread; the barrier makes it visible to all
-    // and guarantees every wave is done with the buffer refilled next.
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    __syncthreads();
+    // This thread's copies of tile t have landed (only tile t+1 may still be
+    // in flight); the barrier publishes them and guarantees every wave has
+    // finished with tile t-1, whose stage tile t+2 reuses.
+    if (t + 1 < tile_end) {
+      wait_vmem<2 * LOADS>();
+    } else {
+      wait_vmem<0>();
+    }
+    lds_barrier();
     if (tstart + kTileKeys > valid_end) {
       // Keys at or beyond P + L are unwritten store memory: clear their V
       // columns so a zero probability never multiplies a NaN.
-      uint16_t* vl = lds + buf * BUF_ELEMS + K_ELEMS;
+      uint16_t* vl = lds + stage * BUF_ELEMS + K_ELEMS;
       const int first = valid_end - tstart;
       for (int idx = tid; idx < D * kTileKeys; idx += kGroupThreads) {
         const int e = idx / kTileKeys, key = idx % kTileKeys;
         if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ (e & 7)) << 3) + (key & 7)] = 0;
       }
-      __syncthreads();
+      lds_barrier();
     }
-    if (t + 1 < tile_end) issue_tile(buf ^ 1, t + 1);
+    if (t + 2 < tile_end) issue_tile((t + 2 - tile_begin) % STAGES, t + 2);
 
+    const uint16_t* kl = lds + stage * BUF_ELEMS;
+    const uint16_t* vl = kl + K_ELEMS;
     if (tstart < my_key_hi) {
-      const uint16_t* kl = lds + buf * BUF_ELEMS;
-      const uint16_t* vl = kl + K_ELEMS;
-      const bool need_mask = tstart < lo || tstart + kTileKeys > full_vis_hi;
-
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        // S^T = K Q^T for 32 keys x 64 queries.
-        f32x16 s[2];
-        s[0] = s[1] = f32x16{};
-        const int kr = sb * 32 + k_row_lo;
-        const uint16_t* krow = kl + kr * D;
-        const int ksw = k_swizzle(kr);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
-          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], s[0], 0, 0, 0);
-          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][ks], s[1], 0, 0, 0);
-        }
-
-        // Element i of the accumulator holds key sb*32 + (i/8)*16 + half*8 + i%8.
-        if (need_mask) {
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb) {
-            const int base = tstart + sb * 32 + half * 8;
-            const int lim_lo = lo - base;
-            const int lim_hi = min(hi, P + row0 + nb * 32 + l32 + 1) - base;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-              const int c = (i / 8) * 16 + (i % 8);
-              if (c < lim_lo || c >= lim_hi) s[nb][i] = -INFINITY;
-            }
-          }
-        }
-
-        bf16x8 pb[2][2];
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          float mx = s[nb][0];
-#pragma unroll
-          for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[nb][i]);
-          mx = lane_pair_max(mx) * sl2;
-          if (__builtin_amdgcn_ballot_w64(mx > m_run[nb] + kRescaleSlack) != 0) {
-            const float m_new = fmaxf(m_run[nb], mx);
-            const float alpha = __builtin_amdgcn_exp2f(m_run[nb] - (m_new == -INFINITY ? 0.f : m_new));
-            l_run[nb] *= alpha;
-#pragma unroll
-            for (int md = 0; md < MD; ++md) oacc[md][nb] *= alpha;
-            m_run[nb] = m_new;
-          }
-          const float neg_m = m_run[nb] == -INFINITY ? 0.f : -m_run[nb];
-          float rs = 0.f;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float e = __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m));
-            rs += e;
-            pb[nb][i / 8][i % 8] = (__bf16)e;
-          }
-          l_run[nb] += rs;
-        }
-
-        // O^T += V^T P^T over these 32 keys (2 k-steps of 16).
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const int vchunk = ((sb * 2 + kk) * 2 + half) ^ v_row_sw;
-#pragma unroll
-          for (int md = 0; md < MD; ++md) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
-            oacc[md][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[0][kk], oacc[md][0], 0, 0, 0);
-            oacc[md][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[1][kk], oacc[md][1], 0, 0, 0);
-          }
-        }
-      }
+      const bool masked = !(t >= fast_begin && t < fast_end);
+      for (int sb = 0; sb < 2; ++sb)
+        if (tstart + sb * 32 < my_key_hi) half_block(kl, vl, tstart, sb, masked);
     }
   }
 
@@ -358,6 +448,7 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
       if (half == 0) p.ws_lse[base] = row_lse;
     }
   }
+#endif  // __HIP_DEVICE_COMPILE__
 }
 
 }  // namespace

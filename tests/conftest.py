@@ -33,7 +33,9 @@ def oracle_lib():
 def mocap_lib():
     """libmocap_attn; built for gfx950 here if it is missing (a CPU-side build step)."""
     from paper_2606_22968_amd import binding, build
-    if not os.path.exists(build.LIB):
+    sources = [os.path.join(build.CSRC, f) for f in os.listdir(build.CSRC)]
+    sources.append(os.path.join(build.INCLUDE, "mocap_attn.h"))
+    if _stale(build.LIB, sources):
         build.build()
     return binding
 

@@ -10,12 +10,15 @@ from paper_2606_22968_amd import synth
 from paper_2606_22968_amd.prefill import ChunkedPrefill
 
 # Parity bar for O (bf16 in, fp32 accumulate): max-abs and mean-abs error
-# against the fp64 oracle.  The LSE bar is this build's reading (the
-# workload statement gives none): fp32 softmax statistics over up to 131072
-# keys stay well inside 1e-3 in absolute natural-log units.
+# against the fp64 oracle.
 O_MAX_ABS = 2e-2
 O_MEAN_ABS = 2e-3
-LSE_MAX_ABS = 1e-3
+# LSE bar, derived from the arithmetic (no bar is stated for it): the row sum
+# adds the bf16-rounded probabilities that also feed P*V, each within 2^-9
+# relative of the exact value, so the sum is within 2^-9 relative and
+# |delta LSE| <= ln(1 + 2^-9) / (1 - 2^-9) ~= 1.96e-3; fp32 exp and
+# accumulation add terms of order 1e-6.
+LSE_MAX_ABS = 2e-3
 
 
 def say(msg):
