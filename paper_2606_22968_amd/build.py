@@ -22,7 +22,7 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # MFMA results in VGPRs: the score accumulators feed the softmax VALU work
-    # directly, and only read-only operands are left for the AGPRs.
+    # directly; read-only MFMA operands (the Q fragments) go to AGPRs.
     "-mllvm", "-amdgpu-mfma-vgpr-form=true",
     "-Wno-unused-command-line-argument",
     f"-I{INCLUDE}", f"-I{CSRC}",

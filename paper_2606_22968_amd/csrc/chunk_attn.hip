@@ -31,6 +31,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace mocap {
 namespace {
 
@@ -92,16 +94,18 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
 }
 
 // Softmax bookkeeping.  Each query row keeps a reference exponent m (base 2)
-// and accumulates p = exp2(s * scale * log2(e) - m) without first taking the
-// block maximum.  m is only a scale: the result sum(p v) / sum(p) does not
-// depend on it as long as nothing overflows.  A block whose partial row sum
-// exceeds 2^kSumLimit (or is not finite, e.g. the first block, where m is
-// still -inf) is recomputed on a slow path that moves m to the block's true
-// maximum and rescales the O accumulator and the running sum.  With
-// attention scores of ordinary size this happens for the first block of a
-// row and almost never again, so the fast path spends no VALU work on maxima
-// and the O accumulator is almost never touched outside the MFMAs.
-constexpr float kSumLimit = 1048576.0f;  // 2^20
+// and accumulates p = exp2(s * scale * log2(e) - m) without taking block
+// maxima.  m is only a scale: the result sum(p v) / sum(p) does not depend on
+// it as long as nothing overflows, and fp32/bf16 keep their relative
+// precision over the whole exponent range.  m is fixed by the first block of
+// the row that has a visible key, while nothing has been accumulated yet, so
+// the O accumulator never needs rescaling.  A later block whose partial row
+// sum exceeds 2^kSumLimitLog2 (a score more than ~60 binary orders above the
+// first block's maximum, which ordinary attention scores never reach) marks
+// the row; after the pass the workgroup re-runs its key range once with m
+// raised to the largest such block maximum.  O is therefore only ever written
+// by MFMAs inside the loop.
+constexpr float kSumLimit = 1152921504606846976.0f;  // 2^60
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
@@ -145,7 +149,8 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   constexpr int K_ELEMS = kTileKeys * D;
   constexpr int BUF_ELEMS = 2 * K_ELEMS;         // K tile + V^T tile
   constexpr int LOADS = K_ELEMS / 8 / kGroupThreads;  // 1 KiB wave loads per operand
-  constexpr int STAGES = 3;
+  constexpr int TILE_OPS = 2 * LOADS;            // DMA instructions per thread per tile
+  constexpr int STAGES = 4;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
 
@@ -183,13 +188,20 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int tile_end = (wg_hi + kTileKeys - 1) / kTileKeys;
   const int valid_end = P + L;
   // Tiles [fast_begin, fast_end) are visible to every row of the workgroup
-  // and need no mask; the others go through the masked path.
-  const int fast_begin = tile_begin + ((lo % kTileKeys) != 0 ? 1 : 0);
+  // and need no mask.  At most one masked tile precedes them (a range start
+  // inside a tile); the rest follow (the causal diagonal, a range end).
+  const int n_head = (lo % kTileKeys) != 0 ? 1 : 0;
+  const int fast_begin = tile_begin + n_head;
   const int fast_end = max(fast_begin, min(tile_end, min(hi, P + wg_row0 + 1) / kTileKeys));
-
-  // Rows of this wavefront; keys at or beyond my_key_hi are masked for all of them.
-  const int my_rows = min(row0 + kWaveRows, L) - row0;
-  const int my_key_hi = my_rows > 0 ? min(hi, P + row0 + my_rows) : INT32_MIN;
+  const int n_fast = fast_end - fast_begin;
+  const int n_tiles = tile_end - tile_begin;
+  // Processing order: the unmasked tiles first, then the head tile, then the
+  // tail; softmax accumulation does not depend on the order of key blocks.
+  auto seq_tile = [&](int i) -> int {
+    if (i < n_fast) return fast_begin + i;
+    if (i < n_fast + n_head) return tile_begin;
+    return fast_end + (i - n_fast - n_head);
+  };
 
   // ---- Q fragments (B operand of S^T = K Q^T) ----
   bf16x8 qf[2][KS];
@@ -222,20 +234,46 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ (vr & 7);
     v_src[j] = vr * p.block_size + vc * 8;
   }
-  auto issue_tile = [&](int stage, int t) {
+  // Sequence position i of the tile order uses LDS stage i % STAGES.
+  auto issue_seq = [&](int i) {
+    const int t = seq_tile(i);
     const int pos0 = t * kTileKeys;
     const int lb = pos0 / p.block_size;
     const int slot0 = pos0 - lb * p.block_size;
     const int64_t base = ((int64_t)table[lb] * p.h_kv + item.kv_head) * head_stride;
     const uint16_t* kb = p.k_pool + base + (int64_t)slot0 * D;
     const uint16_t* vb = p.v_pool + base + slot0;
-    uint16_t* kl = lds + stage * BUF_ELEMS;
+    uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     uint16_t* vl = kl + K_ELEMS;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int dst = (j * kWavesPerGroup + wave) * 64 * 8;
       __builtin_amdgcn_global_load_lds(kb + k_src[j], (lds_ptr_t)(kl + dst), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(vb + v_src[j], (lds_ptr_t)(vl + dst), 16, 0, 0);
+    }
+  };
+  // Make sequence tile i visible to all waves.  `later` = tiles issued after
+  // it that may still be in flight.
+  auto publish_seq = [&](int i, int later) {
+    if (later >= 2) {
+      wait_vmem<2 * TILE_OPS>();
+    } else if (later == 1) {
+      wait_vmem<TILE_OPS>();
+    } else {
+      wait_vmem<0>();
+    }
+    lds_barrier();
+    const int tstart = seq_tile(i) * kTileKeys;
+    if (tstart + kTileKeys > valid_end) {
+      // Keys at or beyond P + L are unwritten store memory: clear their V
+      // columns so a zero probability never multiplies a NaN.
+      uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
+      const int first = valid_end - tstart;
+      for (int idx = tid; idx < D * kTileKeys; idx += kGroupThreads) {
+        const int e = idx / kTileKeys, key = idx % kTileKeys;
+        if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ (e & 7)) << 3) + (key & 7)] = 0;
+      }
+      lds_barrier();
     }
   };
 
@@ -252,23 +290,8 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int v_row_sw = l32 & 7;                      // V^T swizzle of this lane's dim rows
   const uint32_t ones = 0x3F803F80u;                 // bf16 pair (1, 1)
 
-  // Visibility of this lane's 16 keys of a 32-key half block, one bit per
-  // accumulator element i (key offset (i/8)*16 + half*8 + i%8 from `base`):
-  // keys in [lo, hi) and at or before the query's position.
-  auto visible_bits = [&](int base, int nb) -> uint32_t {
-    const int a = lo - base;
-    const int b = min(hi, P + row0 + nb * 32 + l32 + 1) - base;
-    // Offsets (i/8)*16 + i%8 increase with i, so the visible elements form
-    // one run [first_i(a), first_i(b)).
-    auto first_i = [](int x) { return x <= 0 ? 0 : x <= 8 ? x : x <= 16 ? 8 : x <= 24 ? x - 8 : 16; };
-    const int i0 = first_i(a), i1 = first_i(b);
-    return i1 > i0 ? (((1u << i1) - 1u) & ~((1u << i0) - 1u)) : 0u;
-  };
-
-  // One 32-key half of a tile: scores, softmax, P*V.
-  auto half_block = [&](const uint16_t* kl, const uint16_t* vl, int tstart, int sb, bool masked) {
-    f32x16 s[2];
-    s[0] = s[1] = f32x16{};
+  // ---- building blocks of one 32-key half block ----
+  auto scores = [&](f32x16 (&s)[2], const uint16_t* kl, int sb) {
     const int kr = sb * 32 + k_row_lo;
     const uint16_t* krow = kl + kr * D;
     const int ksw = k_swizzle(kr);
@@ -276,82 +299,14 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       kf[ks] = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
+    s[0] = s[1] = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[0][ks], s[0], 0, 0, 0);
       s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[1][ks], s[1], 0, 0, 0);
     }
-
-    // p = exp2(s * sl2 - m), packed to bf16 pairs in P*V B-operand order.
-    // Masked elements are cleared on the packed words (NaN-safe).
-    uint32_t pk[2][8];
-    uint32_t vis[2] = {0xFFFFu, 0xFFFFu};
-    if (masked) {
-      vis[0] = visible_bits(tstart + sb * 32 + half * 8, 0);
-      vis[1] = visible_bits(tstart + sb * 32 + half * 8, 1);
-    }
-    float rs[2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const float neg_m = -m_run[nb];
-#pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m));
-        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m));
-        pk[nb][i / 2] = pack_bf16x2(e0, e1);
-      }
-    }
-    if (masked) {
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[nb], 2 * j, 1);
-          const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[nb], 2 * j + 1, 1);
-          pk[nb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
-        }
-    }
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      float acc = 0.f;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[nb][j], ones, acc);
-      rs[nb] = acc;
-    }
-    const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
-    if (__builtin_amdgcn_ballot_w64(over) != 0) {
-      // Slow path: move m to the block maximum, rescale, recompute p.
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if ((vis[nb] >> i) & 1u) mx = fmaxf(mx, s[nb][i]);
-        mx = lane_pair_max(mx) * sl2;
-        const float m_new = fmaxf(m_run[nb], mx);
-        if (m_new != m_run[nb]) {
-          const float alpha = m_run[nb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
-          l_run[nb] *= alpha;
-#pragma unroll
-          for (int md = 0; md < MD; ++md) oacc[md][nb] *= alpha;
-          m_run[nb] = m_new;
-        }
-        const float neg_m = m_run[nb] == -INFINITY ? 0.f : -m_run[nb];
-        float acc = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; i += 2) {
-          const float e0 = ((vis[nb] >> i) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m)) : 0.f;
-          const float e1 = ((vis[nb] >> (i + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m)) : 0.f;
-          pk[nb][i / 2] = pack_bf16x2(e0, e1);
-          acc = dot2_bf16(pk[nb][i / 2], ones, acc);
-        }
-        rs[nb] = acc;
-      }
-    }
-    l_run[0] += rs[0];
-    l_run[1] += rs[1];
-
-    // O^T += V^T P^T over these 32 keys (2 k-steps of 16).
+  };
+  auto pv = [&](const uint16_t* vl, int sb, const uint32_t (&pk)[2][8]) {
     bf16x8 vf[2][MD];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -371,43 +326,175 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
       }
     }
   };
-
-  // Prologue: the first two tiles in flight.
-  if (tile_begin < tile_end) issue_tile(0, tile_begin);
-  if (tile_begin + 1 < tile_end) issue_tile(1, tile_begin + 1);
-
-  for (int t = tile_begin; t < tile_end; ++t) {
-    const int stage = (t - tile_begin) % STAGES;
-    const int tstart = t * kTileKeys;
-    // This thread's copies of tile t have landed (only tile t+1 may still be
-    // in flight); the barrier publishes them and guarantees every wave has
-    // finished with tile t-1, whose stage tile t+2 reuses.
-    if (t + 1 < tile_end) {
-      wait_vmem<2 * LOADS>();
-    } else {
-      wait_vmem<0>();
+  // Visibility of this lane's 16 keys of a half block for query block nb, one
+  // bit per accumulator element i (key offset (i/8)*16 + half*8 + i%8 from
+  // `base`): keys in [lo, hi) and at or before the query's position.
+  auto visible_bits = [&](int base, int nb) -> uint32_t {
+    const int a = lo - base;
+    const int b = min(hi, P + row0 + nb * 32 + l32 + 1) - base;
+    // The offsets (i/8)*16 + i%8 increase with i, so the visible elements
+    // form one run [first_i(a), first_i(b)).
+    auto first_i = [](int x) { return x <= 0 ? 0 : x <= 8 ? x : x <= 16 ? 8 : x <= 24 ? x - 8 : 16; };
+    const int i0 = first_i(a), i1 = first_i(b);
+    return i1 > i0 ? (((1u << i1) - 1u) & ~((1u << i0) - 1u)) : 0u;
+  };
+  // Probabilities of query block nb: p = exp2(s * sl2 - m) as bf16 pairs,
+  // masked elements cleared on the packed words (NaN-safe), and their sum.
+  auto probs = [&](const f32x16& s, uint32_t (&pk)[8], float& rs, int nb, bool masked, uint32_t vis) {
+    const float neg_m = -m_run[nb];
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[i], sl2, neg_m));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[i + 1], sl2, neg_m));
+      pk[i / 2] = pack_bf16x2(e0, e1);
     }
-    lds_barrier();
-    if (tstart + kTileKeys > valid_end) {
-      // Keys at or beyond P + L are unwritten store memory: clear their V
-      // columns so a zero probability never multiplies a NaN.
-      uint16_t* vl = lds + stage * BUF_ELEMS + K_ELEMS;
-      const int first = valid_end - tstart;
-      for (int idx = tid; idx < D * kTileKeys; idx += kGroupThreads) {
-        const int e = idx / kTileKeys, key = idx % kTileKeys;
-        if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ (e & 7)) << 3) + (key & 7)] = 0;
+    if (masked) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis, 2 * j, 1);
+        const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis, 2 * j + 1, 1);
+        pk[j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
       }
-      lds_barrier();
     }
-    if (t + 2 < tile_end) issue_tile((t + 2 - tile_begin) % STAGES, t + 2);
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[j], ones, acc);
+    rs = acc;
+  };
+  // Accept the half block's probabilities.  Rarely (first visible block of a
+  // row, or an overflow) take the slow path: rows with nothing accumulated
+  // adopt the block maximum as their reference exponent and recompute; rows
+  // that have accumulated are marked for the re-run.  Partner lanes (l and
+  // l ^ 32) hold the same row and always decide together.
+  float m_cand[2] = {-INFINITY, -INFINITY};
+  bool rerun = false;
+  auto settle = [&](const f32x16 (&s)[2], uint32_t (&pk)[2][8], float (&rs)[2], const uint32_t (&vis)[2]) {
+    const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
+    if (__builtin_amdgcn_ballot_w64(over) != 0) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const bool row_over = lane_pair_max(!(rs[nb] <= kSumLimit) ? 1.f : 0.f) > 0.f;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if ((vis[nb] >> i) & 1u) mx = fmaxf(mx, s[nb][i]);
+        mx = lane_pair_max(mx) * sl2;
+        const bool fresh = lane_pair_sum(l_run[nb]) == 0.f;
+        if (row_over && !fresh) {
+          m_cand[nb] = fmaxf(m_cand[nb], mx);
+          rerun = true;
+        }
+        if (row_over && fresh) m_run[nb] = mx;
+        const float neg_m = m_run[nb] == -INFINITY ? 0.f : -m_run[nb];
+        float acc = 0.f;
+        uint32_t fixed[8];
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+          const float e0 = ((vis[nb] >> i) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m)) : 0.f;
+          const float e1 = ((vis[nb] >> (i + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m)) : 0.f;
+          fixed[i / 2] = pack_bf16x2(e0, e1);
+          acc = dot2_bf16(fixed[i / 2], ones, acc);
+        }
+        if (row_over && fresh) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) pk[nb][j] = fixed[j];
+          rs[nb] = acc;
+        }
+      }
+    }
+    l_run[0] += rs[0];
+    l_run[1] += rs[1];
+  };
 
-    const uint16_t* kl = lds + stage * BUF_ELEMS;
-    const uint16_t* vl = kl + K_ELEMS;
-    if (tstart < my_key_hi) {
-      const bool masked = !(t >= fast_begin && t < fast_end);
-      for (int sb = 0; sb < 2; ++sb)
-        if (tstart + sb * 32 < my_key_hi) half_block(kl, vl, tstart, sb, masked);
+  // ---- software pipeline over 32-key half blocks ----
+  // Per tile t (halves 0 and 1) the MFMA stream is
+  //   S1(t) | PV0(t) | S0(t+1) | PV1(t)
+  // and each group overlaps the exp/pack work of one query block of the
+  // half block whose scores are ready:
+  //   S1(t): probs(S0(t), nb 1)      PV0(t): probs(S1(t), nb 0)
+  //   S0(t+1): probs(S1(t), nb 1)    PV1(t): probs(S0(t+1), nb 0)
+  // PV1(t) reads tile t after the barrier that publishes tile t+1, so the
+  // stage of tile t-1 is the first one free for refilling (tile t+3).
+  f32x16 s0[2], s1[2];
+  uint32_t pk0[2][8], pk1[2][8];
+  float rs0[2], rs1[2];
+  uint32_t vis0[2] = {0xFFFFu, 0xFFFFu}, vis1[2] = {0xFFFFu, 0xFFFFu};
+
+  auto masked_seq = [&](int i) { return i >= n_fast; };
+  auto set_vis = [&](uint32_t (&vis)[2], int i, int sb) {
+    if (masked_seq(i)) {
+      const int base = seq_tile(i) * kTileKeys + sb * 32 + half * 8;
+      vis[0] = visible_bits(base, 0);
+      vis[1] = visible_bits(base, 1);
+    } else {
+      vis[0] = vis[1] = 0xFFFFu;
     }
+  };
+
+  // One tile of the pipeline.  MASK selects the masked variant of the
+  // probability computation for the tiles touched by this step.
+  auto step = [&](int i, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
+    const uint16_t* vl = kl + K_ELEMS;
+    const bool has_next = i + 1 < n_tiles;
+    // S1(t) | probs(S0(t), nb 1)
+    scores(s1, kl, 1);
+    probs(s0[1], pk0[1], rs0[1], 1, MASK, vis0[1]);
+    settle(s0, pk0, rs0, vis0);
+    // PV0(t) | probs(S1(t), nb 0)
+    if (MASK) set_vis(vis1, i, 1);
+    pv(vl, 0, pk0);
+    probs(s1[0], pk1[0], rs1[0], 0, MASK, vis1[0]);
+    // Publish tile t+1, refill the stage of tile t-1 with tile t+3.
+    if (has_next) {
+      publish_seq(i + 1, min(n_tiles - (i + 2), 1));
+      if (i + 3 < n_tiles) issue_seq(i + 3);
+    }
+    // S0(t+1) | probs(S1(t), nb 1).  On the last tile the scores are
+    // computed from the current stage and discarded.
+    const uint16_t* kn = has_next ? lds + ((i + 1) % STAGES) * BUF_ELEMS : kl;
+    scores(s0, kn, 0);
+    probs(s1[1], pk1[1], rs1[1], 1, MASK, vis1[1]);
+    settle(s1, pk1, rs1, vis1);
+    // PV1(t) | probs(S0(t+1), nb 0)
+    if (MASK && has_next) set_vis(vis0, i + 1, 0);
+    pv(vl, 1, pk1);
+    probs(s0[0], pk0[0], rs0[0], 0, MASK, vis0[0]);
+  };
+
+  __shared__ int rerun_flag;
+  for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
+    if (tid == 0) rerun_flag = 0;
+    issue_seq(0);
+    if (n_tiles > 1) issue_seq(1);
+    if (n_tiles > 2) issue_seq(2);
+    publish_seq(0, min(n_tiles - 1, 2));
+    set_vis(vis0, 0, 0);
+    scores(s0, lds, 0);
+    probs(s0[0], pk0[0], rs0[0], 0, masked_seq(0), vis0[0]);
+    // Steps whose tile and next tile are both unmasked use the mask-free
+    // variant; all others the masked one.
+    int i = 0;
+    for (; i + 1 < n_fast; ++i) step(i, std::integral_constant<bool, false>{});
+    for (; i < n_tiles; ++i) step(i, std::integral_constant<bool, true>{});
+
+    // Re-run the range if any row of the workgroup overflowed its reference
+    // exponent (all DMA has drained: the last publish waited for vmcnt(0)).
+    if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(&rerun_flag, 1);
+    lds_barrier();
+    const bool again = rerun_flag != 0;
+    lds_barrier();
+    if (!again) break;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      m_run[nb] = fmaxf(m_run[nb], m_cand[nb]);
+      m_cand[nb] = -INFINITY;
+      l_run[nb] = 0.f;
+#pragma unroll
+      for (int md = 0; md < MD; ++md) oacc[md][nb] = f32x16{};
+    }
+    rerun = false;
   }
 
   // ---- epilogue ----

@@ -14,11 +14,12 @@ from paper_2606_22968_amd.prefill import ChunkedPrefill
 O_MAX_ABS = 2e-2
 O_MEAN_ABS = 2e-3
 # LSE bar, derived from the arithmetic (no bar is stated for it): the row sum
-# adds the bf16-rounded probabilities that also feed P*V, each within 2^-9
-# relative of the exact value, so the sum is within 2^-9 relative and
-# |delta LSE| <= ln(1 + 2^-9) / (1 - 2^-9) ~= 1.96e-3; fp32 exp and
-# accumulation add terms of order 1e-6.
-LSE_MAX_ABS = 2e-3
+# adds the bf16-rounded probabilities that also feed P*V.  bf16 keeps 8
+# significant bits, so each rounded probability is within 2^-8 relative of
+# the exact one, the sum is within 2^-8 relative, and
+# |delta LSE| <= ln(1 + 2^-8) / (1 - 2^-8) ~= 3.91e-3 (reached when one key
+# dominates a row); fp32 exp and accumulation add terms of order 1e-5.
+LSE_MAX_ABS = 4e-3
 
 
 def say(msg):
