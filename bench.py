@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--splits", type=int, default=0, help="0 = library's automatic split plan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=16, help="oracle rows per (chunk, head)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (a known-size "
+                         "kernel for scaling a profiler's FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -174,6 +177,14 @@ def main():
             "includes_merge_launches": split_chunks > 0,
         },
     }
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, lengths, args.cpu_rows)

@@ -110,14 +110,20 @@ constexpr float kSumLimit = 1152921504606846976.0f;  // 2^60
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
 
-// LDS layout of one stage (no padding; 16-byte chunks XOR-swizzled so the
-// MFMA operand reads of 8 consecutive lanes hit 8 different 16-byte bank
-// groups):
+// LDS layout of one stage (no padding; 16-byte chunks XOR-swizzled).  A
+// ds_read_b128 serves 16 lanes at a time from 64 four-byte banks, so each run
+// of 16 lanes must touch 16 different 16-byte bank groups of a 256-byte
+// window:
 //   K tile  [64 keys][D]      chunk c of key row r stored at c ^ k_swizzle(r)
-//   V tile  [D][64 keys]      chunk c of dim row e stored at c ^ (e & 7)
-// K operand reads take rows key_row_order(0..7) = {0,1,2,3,8,9,10,11} per
-// 8 lanes; k_swizzle separates r from r + 8.
-__device__ __forceinline__ int k_swizzle(int r) { return (r & 7) ^ ((r >> 1) & 4); }
+//   V tile  [D][64 keys]      chunk c of dim row e stored at c ^ v_swizzle(e)
+// K operand reads take 16 distinct rows per 16 lanes (key_row_order is a
+// permutation of each aligned group of 16); V operand reads take 16
+// consecutive dim rows of 128 bytes, two per 256-byte window.
+template <int D>
+__device__ __forceinline__ int k_swizzle(int r) {
+  return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+__device__ __forceinline__ int v_swizzle(int e) { return (e >> 1) & 7; }
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
@@ -229,9 +235,9 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
     const int chunk = (j * kWavesPerGroup + wave) * 64 + lane;
-    const int kr = chunk / K_ROW_CHUNKS, kc = (chunk % K_ROW_CHUNKS) ^ k_swizzle(kr);
+    const int kr = chunk / K_ROW_CHUNKS, kc = (chunk % K_ROW_CHUNKS) ^ k_swizzle<D>(kr);
     k_src[j] = kr * D + kc * 8;
-    const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ (vr & 7);
+    const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ v_swizzle(vr);
     v_src[j] = vr * p.block_size + vc * 8;
   }
   // Sequence position i of the tile order uses LDS stage i % STAGES.
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
       const int first = valid_end - tstart;
       for (int idx = tid; idx < D * kTileKeys; idx += kGroupThreads) {
         const int e = idx / kTileKeys, key = idx % kTileKeys;
-        if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ (e & 7)) << 3) + (key & 7)] = 0;
+        if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ v_swizzle(e)) << 3) + (key & 7)] = 0;
       }
       lds_barrier();
     }
@@ -287,14 +293,14 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   float l_run[2] = {0.f, 0.f};
   const float sl2 = p.scale_log2;
   const int k_row_lo = key_row_order(l32);          // K row within a 32-key half
-  const int v_row_sw = l32 & 7;                      // V^T swizzle of this lane's dim rows
+  const int v_row_sw = v_swizzle(l32);               // V^T swizzle of this lane's dim rows
   const uint32_t ones = 0x3F803F80u;                 // bf16 pair (1, 1)
 
   // ---- building blocks of one 32-key half block ----
   auto scores = [&](f32x16 (&s)[2], const uint16_t* kl, int sb) {
     const int kr = sb * 32 + k_row_lo;
     const uint16_t* krow = kl + kr * D;
-    const int ksw = k_swizzle(kr);
+    const int ksw = k_swizzle<D>(kr);
     bf16x8 kf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
