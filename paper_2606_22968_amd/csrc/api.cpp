@@ -13,8 +13,8 @@
 namespace {
 
 using mocap::kTileKeys;
-using mocap::kWaveRows;
-using mocap::kWavesPerGroup;
+using mocap::kAttnWaveRows;
+using mocap::kAttnWaves;
 
 constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxPositions = ((int64_t)1 << 31) - 128;
@@ -85,7 +85,7 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
                        int32_t head_dim, int32_t num_splits, Plan* plan) {
   const int group = h_q / h_kv;
   plan->hp = heads_per_wg(group);
-  const int rows_per_wg = kWaveRows * (kWavesPerGroup / plan->hp);
+  const int rows_per_wg = kAttnWaveRows * (kAttnWaves / plan->hp);
   plan->row_groups = (int)((chunk_len + rows_per_wg - 1) / rows_per_wg);
   const int64_t base = (int64_t)(h_q / plan->hp) * plan->row_groups;
   if (base > (int64_t)1 << 24) return MOCAP_ERR_UNSUPPORTED;

@@ -5,13 +5,18 @@
 // grows with its prefix as Eq. (1) of Section 3.2 describes.
 //
 // Kernel structure
-//   * A workgroup is 4 wavefronts.  Each wavefront owns 64 query rows of one
-//     query head, kept in registers as the B operand of the score product.
-//     The 4 wavefronts of a workgroup share one KV head (GQA packing): each
-//     K/V tile staged in LDS serves all of them.
+//   * A workgroup is 8 wavefronts, two per SIMD, each within 256 registers.
+//     Each wavefront owns 32 query rows of one query head, kept in registers
+//     as the B operand of the score product.  All wavefronts of a workgroup
+//     share one KV head (GQA packing), so each K/V tile staged in LDS serves
+//     every query head of the group.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
-//     (global_load_lds_dwordx4, no staging registers) into two stages: tile
-//     t+1 is in flight while tile t is consumed; one barrier per tile.
+//     (global_load_lds_dwordx4, no staging registers) into a 4-stage ring,
+//     prefetched two tiles ahead, one workgroup barrier per tile.
+//   * Ping-pong: waves 0-3 meet the barrier of tile k before their scores of
+//     tile k, waves 4-7 in the middle of their softmax of tile k-1, so the two
+//     waves on each SIMD stay half a tile apart and one's exp/pack VALU work
+//     overlaps the other's MFMAs.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane's accumulator then holds one query and
 //     16 keys, so row statistics need one cross-half exchange
@@ -20,18 +25,19 @@
 //     (bits 2 and 3 of the row index exchanged) so that each lane's 8
 //     probabilities of a P*V step belong to 8 consecutive keys, which are 16
 //     contiguous bytes of the key-contiguous V layout.
-//   * Online softmax in base 2 with scale*log2(e) folded into one FMA.
+//   * Softmax in base 2 with scale*log2(e) folded into one FMA, without block
+//     maxima (see the bookkeeping note below); the row sum adds the bf16
+//     probabilities with v_dot2, so numerator and denominator agree.
 //   * Only tiles that straddle the causal diagonal or a range edge are
-//     masked; tiles entirely above the diagonal are never visited.  Keys at or
-//     beyond P+L (unwritten store memory) are zero-filled in LDS so a masked
-//     probability of 0 never meets a NaN.
+//     masked (a per-lane bit mask applied to the packed probabilities); tiles
+//     entirely above the diagonal are never visited.  Keys at or beyond P+L
+//     (unwritten store memory) are zero-filled in LDS so a masked probability
+//     of 0 never meets a NaN.
 //   * Optional split of the prefix into ranges: each range writes normalised
 //     fp32 partials and their log-sum-exp; lse_merge.hip combines them.
 #include "internal.h"
 
 #include <math.h>
-
-#include <type_traits>
 
 namespace mocap {
 namespace {
@@ -100,7 +106,7 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
 // precision over the whole exponent range.  m is fixed by the first block of
 // the row that has a visible key, while nothing has been accumulated yet, so
 // the O accumulator never needs rescaling.  A later block whose partial row
-// sum exceeds 2^kSumLimitLog2 (a score more than ~60 binary orders above the
+// sum exceeds kSumLimit = 2^60 (a score more than ~60 binary orders above the
 // first block's maximum, which ordinary attention scores never reach) marks
 // the row; after the pass the workgroup re-runs its key range once with m
 // raised to the largest such block maximum.  O is therefore only ever written
@@ -144,21 +150,20 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const AttnLaunch p) {
-  // Device pass only: the host pass needs just the launch stub, and these
-  // gfx950 builtins do not exist for the host target.
+__global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnLaunch p) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int KS = D / 16;                     // k-steps of the score product
-  constexpr int MD = D / 32;                     // 32-wide blocks of the head dim
-  constexpr int K_ROW_CHUNKS = D / 8;            // 16-byte chunks per K row
-  constexpr int V_ROW_CHUNKS = kTileKeys / 8;    // 16-byte chunks per V^T row
+  constexpr int KS = D / 16;
+  constexpr int MD = D / 32;
+  constexpr int K_ROW_CHUNKS = D / 8;
+  constexpr int V_ROW_CHUNKS = kTileKeys / 8;
   constexpr int K_ELEMS = kTileKeys * D;
-  constexpr int BUF_ELEMS = 2 * K_ELEMS;         // K tile + V^T tile
-  constexpr int LOADS = K_ELEMS / 8 / kGroupThreads;  // 1 KiB wave loads per operand
-  constexpr int TILE_OPS = 2 * LOADS;            // DMA instructions per thread per tile
+  constexpr int BUF_ELEMS = 2 * K_ELEMS;
+  constexpr int LOADS = K_ELEMS / 8 / kAttnThreads;
+  constexpr int TILE_OPS = 2 * LOADS;
   constexpr int STAGES = 4;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
+  __shared__ int rerun_flag;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -170,13 +175,12 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int P = p.prefix_len;
   const int L = p.chunk_len;
   const int hp = p.heads_per_wg;
-  const int blocks_per_wg = kWavesPerGroup / hp;
+  const int blocks_per_wg = kAttnWaves / hp;
   const int head = item.head0 + (wave % hp);
-  const int wg_row0 = item.row_group * blocks_per_wg * kWaveRows;
-  const int row0 = wg_row0 + (wave / hp) * kWaveRows;
-  const int wg_row_end = min(L, (item.row_group + 1) * blocks_per_wg * kWaveRows);
+  const int wg_row0 = item.row_group * blocks_per_wg * kAttnWaveRows;
+  const int row0 = wg_row0 + (wave / hp) * kAttnWaveRows;
+  const int wg_row_end = min(L, (item.row_group + 1) * blocks_per_wg * kAttnWaveRows);
 
-  // Key range [lo, hi) of this launch item.
   int lo, hi;
   if (p.n_ranges == 1) {
     lo = 0;
@@ -193,54 +197,42 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
   const int tile_begin = lo / kTileKeys;
   const int tile_end = (wg_hi + kTileKeys - 1) / kTileKeys;
   const int valid_end = P + L;
-  // Tiles [fast_begin, fast_end) are visible to every row of the workgroup
-  // and need no mask.  At most one masked tile precedes them (a range start
-  // inside a tile); the rest follow (the causal diagonal, a range end).
   const int n_head = (lo % kTileKeys) != 0 ? 1 : 0;
   const int fast_begin = tile_begin + n_head;
   const int fast_end = max(fast_begin, min(tile_end, min(hi, P + wg_row0 + 1) / kTileKeys));
   const int n_fast = fast_end - fast_begin;
   const int n_tiles = tile_end - tile_begin;
-  // Processing order: the unmasked tiles first, then the head tile, then the
-  // tail; softmax accumulation does not depend on the order of key blocks.
   auto seq_tile = [&](int i) -> int {
     if (i < n_fast) return fast_begin + i;
     if (i < n_fast + n_head) return tile_begin;
     return fast_end + (i - n_fast - n_head);
   };
 
-  // ---- Q fragments (B operand of S^T = K Q^T) ----
-  bf16x8 qf[2][KS];
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int row = row0 + nb * 32 + l32;
+  // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T).
+  bf16x8 qf[KS];
+  {
+    const int row = row0 + l32;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (row < L) {
-        qf[nb][ks] = *reinterpret_cast<const bf16x8*>(
-            p.q + ((int64_t)row * p.h_q + head) * D + ks * 16 + half * 8);
+        qf[ks] = *reinterpret_cast<const bf16x8*>(p.q + ((int64_t)row * p.h_q + head) * D + ks * 16 + half * 8);
       } else {
-        qf[nb][ks] = bf16x8{};
+        qf[ks] = bf16x8{};
       }
     }
   }
 
-  // ---- tile staging: global -> LDS directly (global_load_lds_dwordx4) ----
-  // Wave instruction j writes LDS chunks [(j*4 + wave)*64, +64) of an operand;
-  // lane i fills chunk (j*4 + wave)*64 + i and fetches the global chunk that
-  // the swizzle maps there.  Block-table entries are read with scalar loads.
   const const_i32_ptr table = (const_i32_ptr)p.table;
-  const int64_t head_stride = (int64_t)D * p.block_size;  // elements per (block, head)
-  int k_src[LOADS], v_src[LOADS];  // per-lane element offsets inside a tile
+  const int64_t head_stride = (int64_t)D * p.block_size;
+  int k_src[LOADS], v_src[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int chunk = (j * kWavesPerGroup + wave) * 64 + lane;
+    const int chunk = (j * kAttnWaves + wave) * 64 + lane;
     const int kr = chunk / K_ROW_CHUNKS, kc = (chunk % K_ROW_CHUNKS) ^ k_swizzle<D>(kr);
     k_src[j] = kr * D + kc * 8;
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ v_swizzle(vr);
     v_src[j] = vr * p.block_size + vc * 8;
   }
-  // Sequence position i of the tile order uses LDS stage i % STAGES.
   auto issue_seq = [&](int i) {
     const int t = seq_tile(i);
     const int pos0 = t * kTileKeys;
@@ -253,13 +245,11 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
     uint16_t* vl = kl + K_ELEMS;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      const int dst = (j * kWavesPerGroup + wave) * 64 * 8;
+      const int dst = (j * kAttnWaves + wave) * 64 * 8;
       __builtin_amdgcn_global_load_lds(kb + k_src[j], (lds_ptr_t)(kl + dst), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(vb + v_src[j], (lds_ptr_t)(vl + dst), 16, 0, 0);
     }
   };
-  // Make sequence tile i visible to all waves.  `later` = tiles issued after
-  // it that may still be in flight.
   auto publish_seq = [&](int i, int later) {
     if (later >= 2) {
       wait_vmem<2 * TILE_OPS>();
@@ -271,11 +261,9 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
     lds_barrier();
     const int tstart = seq_tile(i) * kTileKeys;
     if (tstart + kTileKeys > valid_end) {
-      // Keys at or beyond P + L are unwritten store memory: clear their V
-      // columns so a zero probability never multiplies a NaN.
       uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
       const int first = valid_end - tstart;
-      for (int idx = tid; idx < D * kTileKeys; idx += kGroupThreads) {
+      for (int idx = tid; idx < D * kTileKeys; idx += kAttnThreads) {
         const int e = idx / kTileKeys, key = idx % kTileKeys;
         if (key >= first) vl[e * kTileKeys + (((key >> 3) ^ v_swizzle(e)) << 3) + (key & 7)] = 0;
       }
@@ -283,235 +271,178 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
     }
   };
 
-  f32x16 oacc[MD][2];
+  f32x16 oacc[MD];
 #pragma unroll
-  for (int md = 0; md < MD; ++md) {
-    oacc[md][0] = f32x16{};
-    oacc[md][1] = f32x16{};
-  }
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f, m_cand = -INFINITY;
+  bool rerun = false;
   const float sl2 = p.scale_log2;
-  const int k_row_lo = key_row_order(l32);          // K row within a 32-key half
-  const int v_row_sw = v_swizzle(l32);               // V^T swizzle of this lane's dim rows
-  const uint32_t ones = 0x3F803F80u;                 // bf16 pair (1, 1)
+  const int k_row_lo = key_row_order(l32);
+  const int v_row_sw = v_swizzle(l32);
+  const uint32_t ones = 0x3F803F80u;
 
-  // ---- building blocks of one 32-key half block ----
-  auto scores = [&](f32x16 (&s)[2], const uint16_t* kl, int sb) {
-    const int kr = sb * 32 + k_row_lo;
-    const uint16_t* krow = kl + kr * D;
-    const int ksw = k_swizzle<D>(kr);
-    bf16x8 kf[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      kf[ks] = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
-    s[0] = s[1] = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[0][ks], s[0], 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[1][ks], s[1], 0, 0, 0);
-    }
-  };
-  auto pv = [&](const uint16_t* vl, int sb, const uint32_t (&pk)[2][8]) {
-    bf16x8 vf[2][MD];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int vchunk = ((sb * 2 + kk) * 2 + half) ^ v_row_sw;
-#pragma unroll
-      for (int md = 0; md < MD; ++md)
-        vf[kk][md] = *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
-    }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const bf16x8 pb0 = __builtin_bit_cast(bf16x8, u32x4{pk[0][kk * 4], pk[0][kk * 4 + 1], pk[0][kk * 4 + 2], pk[0][kk * 4 + 3]});
-      const bf16x8 pb1 = __builtin_bit_cast(bf16x8, u32x4{pk[1][kk * 4], pk[1][kk * 4 + 1], pk[1][kk * 4 + 2], pk[1][kk * 4 + 3]});
-#pragma unroll
-      for (int md = 0; md < MD; ++md) {
-        oacc[md][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][md], pb0, oacc[md][0], 0, 0, 0);
-        oacc[md][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][md], pb1, oacc[md][1], 0, 0, 0);
-      }
-    }
-  };
-  // Visibility of this lane's 16 keys of a half block for query block nb, one
-  // bit per accumulator element i (key offset (i/8)*16 + half*8 + i%8 from
-  // `base`): keys in [lo, hi) and at or before the query's position.
-  auto visible_bits = [&](int base, int nb) -> uint32_t {
+  auto visible_bits = [&](int base) -> uint32_t {
     const int a = lo - base;
-    const int b = min(hi, P + row0 + nb * 32 + l32 + 1) - base;
-    // The offsets (i/8)*16 + i%8 increase with i, so the visible elements
-    // form one run [first_i(a), first_i(b)).
+    const int b = min(hi, P + row0 + l32 + 1) - base;
     auto first_i = [](int x) { return x <= 0 ? 0 : x <= 8 ? x : x <= 16 ? 8 : x <= 24 ? x - 8 : 16; };
     const int i0 = first_i(a), i1 = first_i(b);
     return i1 > i0 ? (((1u << i1) - 1u) & ~((1u << i0) - 1u)) : 0u;
   };
-  // Probabilities of query block nb: p = exp2(s * sl2 - m) as bf16 pairs,
-  // masked elements cleared on the packed words (NaN-safe), and their sum.
-  auto probs = [&](const f32x16& s, uint32_t (&pk)[8], float& rs, int nb, bool masked, uint32_t vis) {
-    const float neg_m = -m_run[nb];
+
+  // Pieces of one 64-key tile: scores (16 MFMAs), probabilities of each
+  // 32-key half (VALU), settle, P*V (16 MFMAs).
+  f32x16 s[2];
+  uint32_t vis[2] = {0xFFFFu, 0xFFFFu};
+  uint32_t pk[2][8];
+  float rs[2];
+  auto scores = [&](int i, bool masked) {
+    const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
 #pragma unroll
-    for (int i = 0; i < 16; i += 2) {
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[i], sl2, neg_m));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[i + 1], sl2, neg_m));
-      pk[i / 2] = pack_bf16x2(e0, e1);
+    for (int sb = 0; sb < 2; ++sb) {
+      const int kr = sb * 32 + k_row_lo;
+      const uint16_t* krow = kl + kr * D;
+      const int ksw = k_swizzle<D>(kr);
+      s[sb] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
+        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sb], 0, 0, 0);
+      }
+    }
+    vis[0] = vis[1] = 0xFFFFu;
+    if (masked) {
+      const int tstart = seq_tile(i) * kTileKeys;
+      vis[0] = visible_bits(tstart + half * 8);
+      vis[1] = visible_bits(tstart + 32 + half * 8);
+    }
+  };
+  auto probs_half = [&](int sb, bool masked) {
+    const float neg_m = -m_run;
+#pragma unroll
+    for (int i2 = 0; i2 < 16; i2 += 2) {
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, neg_m));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
+      pk[sb][i2 / 2] = pack_bf16x2(e0, e1);
     }
     if (masked) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis, 2 * j, 1);
-        const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis, 2 * j + 1, 1);
-        pk[j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
+        const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[sb], 2 * j, 1);
+        const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[sb], 2 * j + 1, 1);
+        pk[sb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
       }
     }
     float acc = 0.f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[j], ones, acc);
-    rs = acc;
+    for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[sb][j], ones, acc);
+    rs[sb] = acc;
   };
-  // Accept the half block's probabilities.  Rarely (first visible block of a
-  // row, or an overflow) take the slow path: rows with nothing accumulated
-  // adopt the block maximum as their reference exponent and recompute; rows
-  // that have accumulated are marked for the re-run.  Partner lanes (l and
-  // l ^ 32) hold the same row and always decide together.
-  float m_cand[2] = {-INFINITY, -INFINITY};
-  bool rerun = false;
-  auto settle = [&](const f32x16 (&s)[2], uint32_t (&pk)[2][8], float (&rs)[2], const uint32_t (&vis)[2]) {
+  auto settle = [&]() {
     const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
+      const bool row_over = lane_pair_max(over ? 1.f : 0.f) > 0.f;
+      float mx = -INFINITY;
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const bool row_over = lane_pair_max(!(rs[nb] <= kSumLimit) ? 1.f : 0.f) > 0.f;
-        float mx = -INFINITY;
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if ((vis[nb] >> i) & 1u) mx = fmaxf(mx, s[nb][i]);
-        mx = lane_pair_max(mx) * sl2;
-        const bool fresh = lane_pair_sum(l_run[nb]) == 0.f;
-        if (row_over && !fresh) {
-          m_cand[nb] = fmaxf(m_cand[nb], mx);
-          rerun = true;
-        }
-        if (row_over && fresh) m_run[nb] = mx;
-        const float neg_m = m_run[nb] == -INFINITY ? 0.f : -m_run[nb];
-        float acc = 0.f;
-        uint32_t fixed[8];
+        for (int i2 = 0; i2 < 16; ++i2)
+          if ((vis[sb] >> i2) & 1u) mx = fmaxf(mx, s[sb][i2]);
+      mx = lane_pair_max(mx) * sl2;
+      const bool fresh = lane_pair_sum(l_run) == 0.f;
+      if (row_over && !fresh) {
+        m_cand = fmaxf(m_cand, mx);
+        rerun = true;
+      }
+      if (row_over && fresh) {
+        m_run = mx;
+        const float nm = m_run == -INFINITY ? 0.f : -m_run;
 #pragma unroll
-        for (int i = 0; i < 16; i += 2) {
-          const float e0 = ((vis[nb] >> i) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i], sl2, neg_m)) : 0.f;
-          const float e1 = ((vis[nb] >> (i + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[nb][i + 1], sl2, neg_m)) : 0.f;
-          fixed[i / 2] = pack_bf16x2(e0, e1);
-          acc = dot2_bf16(fixed[i / 2], ones, acc);
-        }
-        if (row_over && fresh) {
+        for (int sb = 0; sb < 2; ++sb) {
+          float acc = 0.f;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) pk[nb][j] = fixed[j];
-          rs[nb] = acc;
+          for (int i2 = 0; i2 < 16; i2 += 2) {
+            const float e0 = ((vis[sb] >> i2) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, nm)) : 0.f;
+            const float e1 = ((vis[sb] >> (i2 + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, nm)) : 0.f;
+            pk[sb][i2 / 2] = pack_bf16x2(e0, e1);
+            acc = dot2_bf16(pk[sb][i2 / 2], ones, acc);
+          }
+          rs[sb] = acc;
         }
       }
     }
-    l_run[0] += rs[0];
-    l_run[1] += rs[1];
+    l_run += rs[0] + rs[1];
   };
-
-  // ---- software pipeline over 32-key half blocks ----
-  // Per tile t (halves 0 and 1) the MFMA stream is
-  //   S1(t) | PV0(t) | S0(t+1) | PV1(t)
-  // and each group overlaps the exp/pack work of one query block of the
-  // half block whose scores are ready:
-  //   S1(t): probs(S0(t), nb 1)      PV0(t): probs(S1(t), nb 0)
-  //   S0(t+1): probs(S1(t), nb 1)    PV1(t): probs(S0(t+1), nb 0)
-  // PV1(t) reads tile t after the barrier that publishes tile t+1, so the
-  // stage of tile t-1 is the first one free for refilling (tile t+3).
-  f32x16 s0[2], s1[2];
-  uint32_t pk0[2][8], pk1[2][8];
-  float rs0[2], rs1[2];
-  uint32_t vis0[2] = {0xFFFFu, 0xFFFFu}, vis1[2] = {0xFFFFu, 0xFFFFu};
-
-  auto masked_seq = [&](int i) { return i >= n_fast; };
-  auto set_vis = [&](uint32_t (&vis)[2], int i, int sb) {
-    if (masked_seq(i)) {
-      const int base = seq_tile(i) * kTileKeys + sb * 32 + half * 8;
-      vis[0] = visible_bits(base, 0);
-      vis[1] = visible_bits(base, 1);
-    } else {
-      vis[0] = vis[1] = 0xFFFFu;
+  auto pv = [&](int i) {
+    const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
+#pragma unroll
+    for (int kst = 0; kst < 4; ++kst) {
+      const int sb = kst / 2, kk = kst % 2;
+      const bf16x8 pb = __builtin_bit_cast(
+          bf16x8, u32x4{pk[sb][kk * 4], pk[sb][kk * 4 + 1], pk[sb][kk * 4 + 2], pk[sb][kk * 4 + 3]});
+      const int vchunk = (kst * 2 + half) ^ v_row_sw;
+#pragma unroll
+      for (int md = 0; md < MD; ++md) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
+        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, oacc[md], 0, 0, 0);
+      }
     }
   };
-
-  // One tile of the pipeline.  MASK selects the masked variant of the
-  // probability computation for the tiles touched by this step.
-  auto step = [&](int i, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
-    const uint16_t* vl = kl + K_ELEMS;
-    const bool has_next = i + 1 < n_tiles;
-    // S1(t) | probs(S0(t), nb 1)
-    scores(s1, kl, 1);
-    probs(s0[1], pk0[1], rs0[1], 1, MASK, vis0[1]);
-    settle(s0, pk0, rs0, vis0);
-    // PV0(t) | probs(S1(t), nb 0)
-    if (MASK) set_vis(vis1, i, 1);
-    pv(vl, 0, pk0);
-    probs(s1[0], pk1[0], rs1[0], 0, MASK, vis1[0]);
-    // Publish tile t+1, refill the stage of tile t-1 with tile t+3.
-    if (has_next) {
-      publish_seq(i + 1, min(n_tiles - (i + 2), 1));
-      if (i + 3 < n_tiles) issue_seq(i + 3);
-    }
-    // S0(t+1) | probs(S1(t), nb 1).  On the last tile the scores are
-    // computed from the current stage and discarded.
-    const uint16_t* kn = has_next ? lds + ((i + 1) % STAGES) * BUF_ELEMS : kl;
-    scores(s0, kn, 0);
-    probs(s1[1], pk1[1], rs1[1], 1, MASK, vis1[1]);
-    settle(s1, pk1, rs1, vis1);
-    // PV1(t) | probs(S0(t+1), nb 0)
-    if (MASK && has_next) set_vis(vis0, i + 1, 0);
-    pv(vl, 1, pk1);
-    probs(s0[0], pk0[0], rs0[0], 0, MASK, vis0[0]);
+  // Barrier k publishes tile k and frees the stage of tile k-2, which tile
+  // k+2 refills.  Group A (waves 0-3) meets barrier k before its scores of
+  // tile k; group B (waves 4-7) meets it between the two probability halves
+  // of tile k-1, so B runs one phase behind A and the two waves sharing a
+  // SIMD alternate between MFMA and VALU work.
+  auto barrier_k = [&](int k) {
+    publish_seq(k, min(n_tiles - 1 - k, 1));
+    if (k + 2 < n_tiles) issue_seq(k + 2);
   };
+  const bool group_b = wave >= 4;
 
-  __shared__ int rerun_flag;
   for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
     if (tid == 0) rerun_flag = 0;
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
-    if (n_tiles > 2) issue_seq(2);
-    publish_seq(0, min(n_tiles - 1, 2));
-    set_vis(vis0, 0, 0);
-    scores(s0, lds, 0);
-    probs(s0[0], pk0[0], rs0[0], 0, masked_seq(0), vis0[0]);
-    // Steps whose tile and next tile are both unmasked use the mask-free
-    // variant; all others the masked one.
-    int i = 0;
-    for (; i + 1 < n_fast; ++i) step(i, std::integral_constant<bool, false>{});
-    for (; i < n_tiles; ++i) step(i, std::integral_constant<bool, true>{});
-
-    // Re-run the range if any row of the workgroup overflowed its reference
-    // exponent (all DMA has drained: the last publish waited for vmcnt(0)).
+    if (!group_b) {
+      for (int i = 0; i < n_tiles; ++i) {
+        const bool masked = i >= n_fast;
+        barrier_k(i);
+        scores(i, masked);
+        probs_half(0, masked);
+        probs_half(1, masked);
+        settle();
+        pv(i);
+      }
+    } else {
+      barrier_k(0);
+      for (int i = 0; i < n_tiles; ++i) {
+        const bool masked = i >= n_fast;
+        scores(i, masked);
+        probs_half(0, masked);
+        if (i + 1 < n_tiles) barrier_k(i + 1);
+        probs_half(1, masked);
+        settle();
+        pv(i);
+      }
+    }
     if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(&rerun_flag, 1);
     lds_barrier();
     const bool again = rerun_flag != 0;
     lds_barrier();
     if (!again) break;
+    m_run = fmaxf(m_run, m_cand);
+    m_cand = -INFINITY;
+    l_run = 0.f;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      m_run[nb] = fmaxf(m_run[nb], m_cand[nb]);
-      m_cand[nb] = -INFINITY;
-      l_run[nb] = 0.f;
-#pragma unroll
-      for (int md = 0; md < MD; ++md) oacc[md][nb] = f32x16{};
-    }
+    for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
     rerun = false;
   }
 
-  // ---- epilogue ----
   const bool split = p.n_ranges > 1;
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const float l_tot = lane_pair_sum(l_run[nb]);
-    const int row = row0 + nb * 32 + l32;
-    if (row >= L) continue;
+  const float l_tot = lane_pair_sum(l_run);
+  const int row = row0 + l32;
+  if (row < L) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float row_lse = l_tot > 0.f ? (m_run[nb] + log2f(l_tot)) * kLn2 : -INFINITY;
+    const float row_lse = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     if (!split) {
       uint16_t* orow = p.o + ((int64_t)row * p.h_q + head) * D;
 #pragma unroll
@@ -520,7 +451,7 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
         for (int j = 0; j < 4; ++j) {
           bf16x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (__bf16)(oacc[md][nb][j * 4 + e] * inv);
+          for (int e = 0; e < 4; ++e) v[e] = (__bf16)(oacc[md][j * 4 + e] * inv);
           *reinterpret_cast<bf16x4*>(orow + md * 32 + j * 8 + half * 4) = v;
         }
       }
@@ -534,7 +465,7 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
         for (int j = 0; j < 4; ++j) {
           f32x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = oacc[md][nb][j * 4 + e] * inv;
+          for (int e = 0; e < 4; ++e) v[e] = oacc[md][j * 4 + e] * inv;
           *reinterpret_cast<f32x4*>(orow + md * 32 + j * 8 + half * 4) = v;
         }
       }
@@ -547,7 +478,7 @@ __global__ __launch_bounds__(kGroupThreads, 1) void chunk_attn_kernel(const Attn
 }  // namespace
 
 hipError_t launch_chunk_attn(const AttnLaunch& p, int head_dim, hipStream_t stream) {
-  const dim3 grid(p.total_wgs), block(kGroupThreads);
+  const dim3 grid(p.total_wgs), block(kAttnThreads);
   if (head_dim == 128) {
     hipLaunchKernelGGL(chunk_attn_kernel<128>, grid, block, 0, stream, p);
   } else {

@@ -8,12 +8,14 @@
 namespace mocap {
 
 constexpr int kTileKeys = 64;          // keys per KV tile (LDS stage)
-constexpr int kWaveRows = 64;          // query rows owned by one wavefront
-constexpr int kWavesPerGroup = 4;      // wavefronts per workgroup
+constexpr int kAttnWaves = 8;          // wavefronts per attention workgroup
+constexpr int kAttnWaveRows = 32;      // query rows owned by one attention wavefront
+constexpr int kAttnThreads = 64 * kAttnWaves;
+constexpr int kWavesPerGroup = 4;      // wavefronts per workgroup of the other kernels
 constexpr int kGroupThreads = 64 * kWavesPerGroup;
 
 // One launch of the attention kernel: every workgroup owns `heads_per_wg`
-// query heads of one GQA group times `64 * 4 / heads_per_wg` query rows, for
+// query heads of one GQA group times `32 * 8 / heads_per_wg` query rows, for
 // one KV range.
 struct AttnLaunch {
   const uint16_t* q;        // bf16 [L][Hq][D]
