@@ -46,6 +46,24 @@ def parse():
     return ap.parse_args()
 
 
+def recorded_traffic(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated against a device copy), or
+    None when there is none for this workload or the kernel source changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"chunk_attn_{workload.replace('_uniform', '')}_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_22968_amd", "csrc", "chunk_attn.hip")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec.get("kernel_source_sha256"):
+            return None
+    return rec["avg_traffic_bytes_per_launch"]
+
+
 def causal_pairs(lengths):
     total, p = 0, 0
     for n in lengths:
@@ -172,7 +190,8 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": recorded_traffic(w.name),
+            "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE)",
             "launches_per_step": n_chunks,
             "includes_merge_launches": split_chunks > 0,
         },

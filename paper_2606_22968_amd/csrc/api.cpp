@@ -4,9 +4,14 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <functional>
+#include <mutex>
+#include <queue>
+#include <vector>
 
 #include "internal.h"
 
@@ -62,23 +67,115 @@ size_t workspace_for(int n_ranges, int64_t chunk_len, int h_q, int head_dim) {
   return round_up(rows * (size_t)head_dim * sizeof(float), 256) + round_up(rows * sizeof(float), 256);
 }
 
-// Number of KV ranges to use.  Auto mode cuts the prefix until the launch has
-// roughly two workgroups per compute unit, keeping every prefix range at
-// least 8 tiles (512 keys) long.
-int choose_ranges(int64_t prefix_tiles, int base_wgs, int requested, int cu_count) {
+// Time model of one launch, used to choose the number of KV ranges.
+//   * A workgroup costs kTileUs per 64-key tile it visits (scaled by
+//     head_dim / 128) plus kGroupUs of fixed work; one workgroup per compute
+//     unit at a time (the attention kernel's LDS ring fills a CU).
+//   * The launch time is the makespan of longest-first list scheduling of
+//     all workgroups onto the compute units (the kernel orders its work items
+//     longest first), plus, when split, the partial-result traffic (written
+//     by the attention kernel, read by the merge) at kMergeBytesPerUs.
+// The constants were measured on MI355X; only the ranking of candidate
+// plans depends on them.
+constexpr double kTileUs = 2.0;
+constexpr double kGroupUs = 4.0;
+constexpr double kMergeBytesPerUs = 3.0e6;
+constexpr double kLaunchUs = 4.0;
+
+double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int head_dim, int head_blocks_total,
+                          int row_groups, int rows_per_wg, int64_t prefix_tiles, int n_ranges, int slots) {
+  std::vector<double> cost;
+  cost.reserve((size_t)head_blocks_total * row_groups * n_ranges);
+  const double tile_us = kTileUs * head_dim / 128.0;
+  for (int rg = 0; rg < row_groups; ++rg) {
+    const int64_t row_end = std::min<int64_t>(chunk_len, (int64_t)(rg + 1) * rows_per_wg);
+    if (n_ranges == 1) {
+      const int64_t tiles = (prefix_len + row_end + kTileKeys - 1) / kTileKeys;
+      for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back(tiles * tile_us + kGroupUs);
+    } else {
+      const int64_t t0 = prefix_len / kTileKeys;
+      const int64_t t1 = (prefix_len + row_end + kTileKeys - 1) / kTileKeys;
+      for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back((t1 - t0) * tile_us + kGroupUs);
+    }
+  }
+  if (n_ranges > 1) {
+    const int parts = n_ranges - 1;
+    for (int r = 0; r < parts; ++r) {
+      const int64_t tiles = prefix_tiles * (r + 1) / parts - prefix_tiles * r / parts;
+      for (int i = 0; i < head_blocks_total * row_groups; ++i) cost.push_back(tiles * tile_us + kGroupUs);
+    }
+  }
+  std::sort(cost.begin(), cost.end(), std::greater<double>());
+  std::priority_queue<double, std::vector<double>, std::greater<double>> load;
+  for (int i = 0; i < slots; ++i) load.push(0.0);
+  double makespan = 0.0;
+  for (double c : cost) {
+    const double t = load.top() + c;
+    load.pop();
+    load.push(t);
+    makespan = std::max(makespan, t);
+  }
+  double total = makespan + kLaunchUs;
+  if (n_ranges > 1) {
+    const double partial = (double)n_ranges * chunk_len * h_q * (head_dim + 1) * 4.0;
+    total += 2.0 * partial / kMergeBytesPerUs + kLaunchUs;
+  }
+  return total;
+}
+
+struct PlanKey {
+  int64_t prefix_len;
+  int32_t chunk_len, h_q, h_kv, head_dim, requested, slots;
+  bool operator==(const PlanKey& o) const {
+    return prefix_len == o.prefix_len && chunk_len == o.chunk_len && h_q == o.h_q && h_kv == o.h_kv &&
+           head_dim == o.head_dim && requested == o.requested && slots == o.slots;
+  }
+};
+
+// Small cache of automatic choices (a chunk loop asks for the same shape in
+// mocap_chunk_attn_workspace_size and in mocap_chunk_attn).
+std::mutex g_plan_mutex;
+constexpr int kPlanCache = 64;
+PlanKey g_plan_keys[kPlanCache];
+int g_plan_values[kPlanCache];
+int g_plan_count = 0, g_plan_next = 0;
+
+// Number of KV ranges to use.  A requested count is clamped to what the
+// prefix allows; 0 picks, among the prefix cut into 1, 2, 4, 8 or 16 ranges
+// of at least 4 tiles (plus the chunk's own range), or no split at all, the
+// plan with the smallest modelled launch time.
+int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int head_dim, int head_blocks_total,
+                  int row_groups, int rows_per_wg, int64_t prefix_tiles, int requested, int slots) {
   if (prefix_tiles <= 0) return 1;
   if (requested >= 1) {
     if (requested == 1) return 1;
     const int64_t parts = requested - 1 < prefix_tiles ? requested - 1 : prefix_tiles;
     return (int)parts + 1;
   }
-  if (base_wgs >= cu_count) return 1;
-  int64_t parts = (2 * (int64_t)cu_count + base_wgs - 1) / base_wgs - 1;
-  const int64_t max_parts = prefix_tiles / 8;
-  if (parts > max_parts) parts = max_parts;
-  if (parts < 1) return 1;
-  if (parts > 64) parts = 64;
-  return (int)parts + 1;
+  const PlanKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, requested, slots};
+  {
+    std::lock_guard<std::mutex> lock(g_plan_mutex);
+    for (int i = 0; i < g_plan_count; ++i)
+      if (g_plan_keys[i] == key) return g_plan_values[i];
+  }
+  int best = 1;
+  double best_us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
+                                      rows_per_wg, prefix_tiles, 1, slots);
+  const int64_t max_parts = std::min<int64_t>(16, prefix_tiles / 4);
+  for (int64_t parts = 1; parts <= max_parts; parts *= 2) {
+    const double us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
+                                         rows_per_wg, prefix_tiles, (int)parts + 1, slots);
+    if (us < best_us * 0.98) {  // a split must pay for itself clearly
+      best_us = us;
+      best = (int)parts + 1;
+    }
+  }
+  std::lock_guard<std::mutex> lock(g_plan_mutex);
+  g_plan_keys[g_plan_next] = key;
+  g_plan_values[g_plan_next] = best;
+  g_plan_next = (g_plan_next + 1) % kPlanCache;
+  if (g_plan_count < kPlanCache) ++g_plan_count;
+  return best;
 }
 
 mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
@@ -96,7 +193,8 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
     const mocap_status st = device_cu_count(&cus);
     if (st != MOCAP_OK) return st;
   }
-  plan->n_ranges = choose_ranges(plan->prefix_tiles, plan->base_wgs, num_splits, cus);
+  plan->n_ranges = choose_ranges(prefix_len, chunk_len, h_q, h_kv, head_dim, h_q / plan->hp, plan->row_groups,
+                                 rows_per_wg, plan->prefix_tiles, num_splits, cus);
   plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
   return MOCAP_OK;
 }
