@@ -297,17 +297,28 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   float rs[2];
   auto scores = [&](int i, bool masked) {
     const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
+    const uint16_t* krow0 = kl + k_row_lo * D;
+    const uint16_t* krow1 = kl + (32 + k_row_lo) * D;
+    const int ksw0 = k_swizzle<D>(k_row_lo), ksw1 = k_swizzle<D>(32 + k_row_lo);
+    // The two 32-key halves are independent accumulation chains; their K
+    // fragments are read two k-steps ahead of the MFMAs that use them.
+    auto kfrag = [&](const uint16_t* krow, int ksw, int ks) {
+      return *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
+    };
+    bf16x8 a0[KS], a1[KS];
+    a0[0] = kfrag(krow0, ksw0, 0);
+    a1[0] = kfrag(krow1, ksw1, 0);
+    a0[1] = kfrag(krow0, ksw0, 1);
+    a1[1] = kfrag(krow1, ksw1, 1);
+    s[0] = s[1] = f32x16{};
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const int kr = sb * 32 + k_row_lo;
-      const uint16_t* krow = kl + kr * D;
-      const int ksw = k_swizzle<D>(kr);
-      s[sb] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
-        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sb], 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 2 < KS) {
+        a0[ks + 2] = kfrag(krow0, ksw0, ks + 2);
+        a1[ks + 2] = kfrag(krow1, ksw1, ks + 2);
       }
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[ks], qf[ks], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], qf[ks], s[1], 0, 0, 0);
     }
     vis[0] = vis[1] = 0xFFFFu;
     if (masked) {
@@ -374,17 +385,27 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   };
   auto pv = [&](int i) {
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
+    auto vfrag = [&](int kst, int md) {
+      const int vchunk = (kst * 2 + half) ^ v_row_sw;
+      return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
+    };
+    // V fragments of the next 16-key step are read while the current step's
+    // four (independent) MFMAs run.
+    bf16x8 vf[4][MD];
+#pragma unroll
+    for (int md = 0; md < MD; ++md) vf[0][md] = vfrag(0, md);
 #pragma unroll
     for (int kst = 0; kst < 4; ++kst) {
+      if (kst + 1 < 4) {
+#pragma unroll
+        for (int md = 0; md < MD; ++md) vf[kst + 1][md] = vfrag(kst + 1, md);
+      }
       const int sb = kst / 2, kk = kst % 2;
       const bf16x8 pb = __builtin_bit_cast(
           bf16x8, u32x4{pk[sb][kk * 4], pk[sb][kk * 4 + 1], pk[sb][kk * 4 + 2], pk[sb][kk * 4 + 3]});
-      const int vchunk = (kst * 2 + half) ^ v_row_sw;
 #pragma unroll
-      for (int md = 0; md < MD; ++md) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
-        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, oacc[md], 0, 0, 0);
-      }
+      for (int md = 0; md < MD; ++md)
+        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kst][md], pb, oacc[md], 0, 0, 0);
     }
   };
   // Barrier k publishes tile k and frees the stage of tile k-2, which tile
