@@ -25,8 +25,8 @@
  *
  * Conventions shared by every call
  *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
- *     allocates no memory and keeps no state across calls except a per-device
- *     cache of the compute-unit count.
+ *     allocates no device memory and keeps no state across calls except small
+ *     caches (per-device compute-unit count, recent automatic split choices).
  *   - Calls enqueue work on `stream` (a hipStream_t passed as void*; NULL is
  *     the default stream) and return without synchronising.  A device-side
  *     fault shows up at the caller's next synchronisation.
@@ -174,6 +174,42 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
  */
 mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align, int32_t balanced,
                               int32_t* lengths_out);
+
+/*
+ * mocap_lbcp_plan -- first stage of latency-balanced chunk partitioning
+ * (Section 4.2, Alg. 1, the dynamic-programming initialisation), host only.
+ *
+ * Chooses num_chunks chunk lengths, each a positive multiple of align, that
+ * sum to seq_len, by the dynamic program of Alg. 1: scanning chunk index m
+ * from num_chunks down to 1, start s from the end down to 0 and length k
+ * upwards, the cost t of a chunk of k starting at s is combined with the best
+ * suffix state (m+1, s+k) into t'_max = max(t_max, t) and t'_sum = t_sum + t,
+ * and the candidate minimising t'_sum + (num_stages - 1) * t'_max is kept.
+ * The suffix boundary, which the paper leaves implicit, is t = 0 at
+ * (num_chunks + 1, seq_len) and infeasible elsewhere.
+ *
+ * EvaluateChunk is the deterministic compute-latency model
+ *   t(c, p) = cost_pair * (c p + c (c + 1) / 2) + cost_token * c + cost_chunk
+ * for a chunk of c tokens behind p tokens: c p + c (c + 1) / 2 is the exact
+ * number of causally visible (query, key) pairs, the attention term of
+ * Eq. (1); cost_token covers work proportional to c (the GEMM term of
+ * Eq. (1), appends); cost_chunk is a fixed cost per chunk.  The
+ * coefficients are typically fitted to measured mocap_chunk_attn latency.
+ *
+ *   seq_len      S, a positive multiple of align
+ *   num_chunks   M >= 1, with M * align <= S
+ *   num_stages   N >= 1, pipeline stages of Alg. 1's objective
+ *   lengths_out  host int32 [num_chunks]
+ *   t_max_out, t_sum_out   (may be NULL) the plan's largest chunk cost and
+ *                sum of chunk costs under the model
+ * Work is O(M (S/align)^2); the call allocates host memory for its tables.
+ * Errors: INVALID_ARG for non-positive sizes, a null lengths_out, S not a
+ * multiple of align, M * align > S or negative/non-finite coefficients;
+ * UNSUPPORTED when M (S/align)^2 exceeds 2^31 (the table would be too slow).
+ */
+mocap_status mocap_lbcp_plan(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                             double cost_pair, double cost_token, double cost_chunk,
+                             int32_t* lengths_out, double* t_max_out, double* t_sum_out);
 
 /* A static, human-readable name for a status code. */
 const char* mocap_status_string(mocap_status status);

@@ -27,6 +27,7 @@ EXPORTED = (
     "mocap_chunk_attn_workspace_size",
     "mocap_chunk_attn",
     "mocap_chunk_plan",
+    "mocap_lbcp_plan",
     "mocap_status_string",
 )
 
@@ -78,6 +79,11 @@ def load_library():
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
         ctypes.c_int32, ctypes.c_void_p]
+    lib.mocap_lbcp_plan.restype = st
+    lib.mocap_lbcp_plan.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+        ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_int32),
+        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     lib.mocap_chunk_plan.restype = st
     lib.mocap_chunk_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -189,3 +195,15 @@ def mocap_chunk_plan(seq_len: int, num_chunks: int, align: int = 128, balanced: 
     _check(load_library().mocap_chunk_plan(int(seq_len), int(num_chunks), int(align), int(bool(balanced)), out),
            "mocap_chunk_plan")
     return list(out)
+
+
+def mocap_lbcp_plan(seq_len: int, num_chunks: int, num_stages: int, align: int, cost_pair: float,
+                    cost_token: float = 0.0, cost_chunk: float = 0.0):
+    """Returns (lengths, t_max, t_sum) of the dynamic-programming plan."""
+    out = (ctypes.c_int32 * num_chunks)()
+    t_max = ctypes.c_double(0.0)
+    t_sum = ctypes.c_double(0.0)
+    _check(load_library().mocap_lbcp_plan(int(seq_len), int(num_chunks), int(num_stages), int(align),
+                                          float(cost_pair), float(cost_token), float(cost_chunk), out,
+                                          ctypes.byref(t_max), ctypes.byref(t_sum)), "mocap_lbcp_plan")
+    return list(out), t_max.value, t_sum.value

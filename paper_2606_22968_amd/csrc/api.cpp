@@ -388,4 +388,58 @@ mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align
   return MOCAP_OK;
 }
 
+mocap_status mocap_lbcp_plan(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                             double cost_pair, double cost_token, double cost_chunk,
+                             int32_t* lengths_out, double* t_max_out, double* t_sum_out) {
+#pragma clang fp contract(off)
+  if (seq_len <= 0 || num_chunks <= 0 || num_stages <= 0 || align <= 0 || lengths_out == nullptr)
+    return MOCAP_ERR_INVALID_ARG;
+  if (seq_len % align != 0 || (int64_t)num_chunks * align > seq_len) return MOCAP_ERR_INVALID_ARG;
+  if (!(cost_pair >= 0.0) || !(cost_token >= 0.0) || !(cost_chunk >= 0.0) || !std::isfinite(cost_pair) ||
+      !std::isfinite(cost_token) || !std::isfinite(cost_chunk))
+    return MOCAP_ERR_INVALID_ARG;
+  const int64_t U = seq_len / align;  // positions in units of align
+  if ((double)num_chunks * (double)U * (double)U > 2147483648.0) return MOCAP_ERR_UNSUPPORTED;
+  if (U > 0x7fffffff / align) return MOCAP_ERR_INVALID_ARG;
+  const int M = num_chunks;
+  const double stages_m1 = (double)(num_stages - 1);
+  const double inf = INFINITY;
+  // Tables over chunk index m = 1 .. M+1 and start u = 0 .. U.
+  std::vector<double> tmax((size_t)(M + 2) * (U + 1), inf), tsum((size_t)(M + 2) * (U + 1), inf);
+  std::vector<int32_t> ss((size_t)(M + 2) * (U + 1), 0);
+  auto at = [&](int m, int64_t u) { return (size_t)m * (U + 1) + (size_t)u; };
+  tmax[at(M + 1, U)] = 0.0;
+  tsum[at(M + 1, U)] = 0.0;
+  for (int m = M; m >= 1; --m) {
+    for (int64_t s = U - 1; s >= 0; --s) {
+      double best_obj = inf;
+      for (int64_t k = 1; k <= U - s - (M - m); ++k) {
+        const size_t nxt = at(m + 1, s + k);
+        if (tsum[nxt] == inf) continue;  // infeasible suffix
+        const double c = (double)(k * align), p = (double)(s * align);
+        const double t = cost_pair * (c * p + c * (c + 1.0) / 2.0) + cost_token * c + cost_chunk;
+        const double t_max = std::max(tmax[nxt], t);
+        const double t_sum = tsum[nxt] + t;
+        const double obj = t_sum + stages_m1 * t_max;
+        if (obj < best_obj) {
+          best_obj = obj;
+          tmax[at(m, s)] = t_max;
+          tsum[at(m, s)] = t_sum;
+          ss[at(m, s)] = (int32_t)k;
+        }
+      }
+    }
+  }
+  if (tsum[at(1, 0)] == inf) return MOCAP_ERR_INVALID_ARG;
+  int64_t u = 0;
+  for (int m = 1; m <= M; ++m) {
+    const int32_t k = ss[at(m, u)];
+    lengths_out[m - 1] = k * align;
+    u += k;
+  }
+  if (t_max_out) *t_max_out = tmax[at(1, 0)];
+  if (t_sum_out) *t_sum_out = tsum[at(1, 0)];
+  return MOCAP_OK;
+}
+
 }  // extern "C"

@@ -1,0 +1,141 @@
+"""LBCP stage 1 (Section 4.2, Alg. 1): the oracle's dynamic program pinned to
+brute force and closed forms, then the library's C implementation compared
+with it exactly."""
+import math
+import random
+
+import pytest
+
+from oracle import lbcp
+from oracle import plan as oplan
+
+
+def linear(cost_pair, cost_token=0.0, cost_chunk=0.0):
+    return lambda c, p: lbcp.chunk_cost(c, p, cost_pair, cost_token, cost_chunk)
+
+
+# --- oracle pins ----------------------------------------------------------
+
+@pytest.mark.parametrize("S,M,align", [(12, 3, 1), (16, 4, 2), (10, 1, 1), (9, 9, 1), (14, 5, 1)])
+def test_sum_is_invariant_under_linear_model(S, M, align):
+    # Every (query, key) pair of the causal square is visible in exactly one
+    # chunk, so under the linear model the sum of chunk costs is
+    # cost_pair * S (S + 1) / 2 + cost_token * S + M * cost_chunk for ANY plan.
+    lengths, t_max, t_sum = lbcp.lbcp_dp(S, M, 4, align, 3.0, 5.0, 7.0)
+    assert sum(lengths) == S and len(lengths) == M
+    assert all(c > 0 and c % align == 0 for c in lengths)
+    assert t_sum == 3.0 * S * (S + 1) / 2 + 5.0 * S + 7.0 * M
+
+
+@pytest.mark.parametrize("S,M", [(12, 3), (13, 4), (10, 2), (15, 5), (11, 11)])
+@pytest.mark.parametrize("N", [2, 4, 10 ** 9])
+def test_min_max_equals_brute_force(S, M, N):
+    # Integer coefficients keep every cost exact; with a plan-independent sum
+    # the objective t_sum + (N - 1) t_max is minimised exactly by the smallest
+    # attainable largest chunk cost, which brute force finds.
+    ev = linear(2.0, 1.0, 3.0)
+    _, t_max, t_sum = lbcp.lbcp_dp(S, M, N, 1, evaluate=ev)
+    best_max, _ = lbcp.brute_force(S, M, 1, max, ev)
+    assert t_max == best_max
+
+
+@pytest.mark.parametrize("S,M", [(12, 3), (13, 4), (9, 2), (10, 5)])
+def test_single_stage_is_min_sum_for_any_cost(S, M):
+    # N = 1 makes the objective additive, where the dynamic program is exact:
+    # a position-dependent, non-linear cost checks the suffix bookkeeping.
+    def ev(c, p):
+        return c * c * c + 7 * p + ((c * 31 + p * 17) % 11)
+    _, _, t_sum = lbcp.lbcp_dp(S, M, 1, 1, evaluate=ev)
+    best_sum, _ = lbcp.brute_force(S, M, 1, sum, ev)
+    assert t_sum == best_sum
+
+
+@pytest.mark.parametrize("S,M", [(12, 3), (11, 4), (10, 3)])
+def test_huge_stage_count_is_min_max_for_any_cost(S, M):
+    # For N large enough that any difference in the largest chunk cost
+    # outweighs any difference in the sum, the chosen suffix at every state
+    # has the smallest attainable maximum, so the plan's maximum is optimal.
+    def ev(c, p):
+        return c * c + 3 * p + ((c * 13 + p * 7) % 5)
+    _, t_max, _ = lbcp.lbcp_dp(S, M, 10 ** 9, 1, evaluate=ev)
+    best_max, _ = lbcp.brute_force(S, M, 1, max, ev)
+    assert t_max == best_max
+
+
+@pytest.mark.parametrize("N", [1, 3, 8])
+def test_reported_costs_match_plan(N):
+    ev = linear(0.5, 2.0, 1.0)
+    lengths, t_max, t_sum = lbcp.lbcp_dp(64, 5, N, 4, evaluate=ev)
+    costs = lbcp.plan_costs(lengths, ev)
+    assert t_max == max(costs)
+    assert t_sum == pytest.approx(sum(costs), rel=1e-15)
+
+
+def test_token_only_cost_gives_uniform_plan():
+    # With cost proportional to chunk length only, the smallest maximum is the
+    # ceiling of S / M (in align units).
+    lengths, t_max, _ = lbcp.lbcp_dp(40 * 8, 6, 4, 8, 0.0, 1.0, 0.0)
+    assert t_max == math.ceil(40 / 6) * 8
+    assert max(lengths) == math.ceil(40 / 6) * 8
+
+
+def test_pair_cost_tracks_square_root_boundaries():
+    # Under the pair cost alone the balanced chunks have boundaries near
+    # S sqrt(c / M) (the continuous optimum of the balanced plan); the
+    # discrete min-max plan's boundaries stay within a few align units.
+    S, M, align = 2048, 8, 16
+    lengths, _, _ = lbcp.lbcp_dp(S, M, 10 ** 6, align, 1.0)
+    dp_bounds = oplan.prefixes(lengths)[1:]
+    cont = [S * math.sqrt(c / M) for c in range(1, M + 1)]
+    assert all(abs(a - b) <= 3 * align for a, b in zip(dp_bounds, cont))
+    # and its maximum is no worse than the rounded closed-form plan's.
+    closed = oplan.balanced_plan(S, M, align)
+    ev = linear(1.0)
+    assert max(lbcp.plan_costs(lengths, ev)) <= max(lbcp.plan_costs(closed, ev))
+
+
+def test_oracle_catches_planted_index_error():
+    # A suffix looked up one position off must disagree with brute force.
+    def bad_dp(S, M, N):
+        ev = linear(2.0, 1.0, 3.0)
+        # Plant the mistake by evaluating chunks one token behind where they start.
+        return lbcp.lbcp_dp(S, M, N, 1, evaluate=lambda c, p: ev(c, max(p - 1, 0)))
+    _, t_max, _ = bad_dp(13, 4, 10 ** 9)
+    best_max, _ = lbcp.brute_force(13, 4, 1, max, linear(2.0, 1.0, 3.0))
+    assert t_max != best_max
+
+
+# --- library == oracle ----------------------------------------------------
+
+def test_library_matches_oracle_exactly(mocap_lib):
+    from paper_2606_22968_amd import binding
+    rng = random.Random(7)
+    cases = [(2048, 8, 4, 64), (4096, 16, 4, 128), (1024, 5, 1, 32), (1536, 12, 16, 64), (640, 10, 2, 64)]
+    for S, M, N, align in cases:
+        for _ in range(3):
+            cp, ct, cc = rng.uniform(0, 1e-3), rng.uniform(0, 1e-1), rng.uniform(0, 50)
+            got = binding.mocap_lbcp_plan(S, M, N, align, cp, ct, cc)
+            want = lbcp.lbcp_dp(S, M, N, align, cp, ct, cc)
+            assert got[0] == want[0], (S, M, N, align)
+            assert got[1] == want[1] and got[2] == want[2]
+
+
+def test_library_validation(mocap_lib):
+    from paper_2606_22968_amd import binding
+    bad = [
+        dict(seq_len=1000, num_chunks=4, num_stages=4, align=64),   # not a multiple of align
+        dict(seq_len=256, num_chunks=5, num_stages=4, align=64),    # more chunks than units
+        dict(seq_len=256, num_chunks=0, num_stages=4, align=64),
+        dict(seq_len=256, num_chunks=2, num_stages=0, align=64),
+        dict(seq_len=256, num_chunks=2, num_stages=1, align=0),
+    ]
+    for kw in bad:
+        with pytest.raises(binding.MocapError) as e:
+            binding.mocap_lbcp_plan(**kw, cost_pair=1.0)
+        assert e.value.status == binding.MOCAP_ERR_INVALID_ARG
+    for cp in (-1.0, math.inf, math.nan):
+        with pytest.raises(binding.MocapError):
+            binding.mocap_lbcp_plan(256, 2, 2, 64, cp)
+    with pytest.raises(binding.MocapError) as e:
+        binding.mocap_lbcp_plan(1 << 20, 64, 4, 1, 1.0)
+    assert e.value.status == binding.MOCAP_ERR_UNSUPPORTED
