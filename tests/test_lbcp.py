@@ -139,3 +139,40 @@ def test_library_validation(mocap_lib):
     with pytest.raises(binding.MocapError) as e:
         binding.mocap_lbcp_plan(1 << 20, 64, 4, 1, 1.0)
     assert e.value.status == binding.MOCAP_ERR_UNSUPPORTED
+
+
+# --- latency model fit and probe plans (host logic) ----------------------
+
+def test_fit_recovers_known_model():
+    from paper_2606_22968_amd import lbcp as plbcp
+    true = (2.5e-6, 3e-3, 40.0)
+    rng = random.Random(3)
+    samples = []
+    for _ in range(60):
+        c = rng.randrange(128, 32768, 128)
+        p = rng.randrange(0, 131072 - c + 1, 128)
+        t = true[0] * plbcp.visible_pairs(c, p) + true[1] * c + true[2]
+        samples.append((c, p, t * (1 + rng.uniform(-1e-3, 1e-3))))
+    m = plbcp.fit(samples)
+    assert m.cost_pair == pytest.approx(true[0], rel=1e-2)
+    assert m.cost_token == pytest.approx(true[1], rel=0.2)
+    assert m.cost_chunk == pytest.approx(true[2], rel=0.2)
+    assert m.rms_rel_err < 2e-3
+    assert m(4096, 8192) == pytest.approx(lbcp.chunk_cost(4096, 8192, *true), rel=1e-2)
+
+
+def test_fit_keeps_coefficients_non_negative():
+    from paper_2606_22968_amd import lbcp as plbcp
+    # Latency that falls with chunk length would need a negative token cost.
+    samples = [(c, 0, 100.0 - 0.001 * c + 1e-6 * c * c) for c in range(128, 8192, 512)]
+    m = plbcp.fit(samples)
+    assert min(m.cost_pair, m.cost_token, m.cost_chunk) >= 0.0
+
+
+def test_probe_plans_are_valid(mocap_lib):
+    from paper_2606_22968_amd import lbcp as plbcp
+    plans = plbcp.probe_plans(131072, 16, 128, seed=2, n_random=5)
+    assert len(plans) == 7
+    for lengths in plans:
+        assert len(lengths) == 16 and sum(lengths) == 131072
+        assert all(c > 0 and c % 128 == 0 for c in lengths)
