@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b_32k_uniform")
     ap.add_argument("--splits", type=int, default=0, help="0 = library's automatic split plan")
+    ap.add_argument("--remote-fraction", type=float, default=0.0,
+                    help="hold the KV of the first fraction of the sequence (whole blocks) in a second store, "
+                         "as a debtor stage's remote portion, and read it with the two-store call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=16, help="oracle rows per (chunk, head)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -118,8 +121,15 @@ def main():
     q, k, v = synth.make_qkv(w.seed, w.seq_len, w.h_q, w.h_kv, w.head_dim)
     n_blocks = (w.seq_len + w.block_size - 1) // w.block_size
     table = synth.permuted_table(n_blocks, w.perm_seed) if w.permuted else None
+    remote = None
+    if args.remote_fraction > 0:
+        end = int(args.remote_fraction * w.seq_len) // w.block_size * w.block_size
+        # A chunk boundary inside the range must sit on a 64-key tile: move the end back to one.
+        while any(0 < p < end and p % 64 for p in synth.prefixes(lengths)):
+            end -= w.block_size
+        remote = (0, max(end, 0))
     runner = ChunkedPrefill(w.h_q, w.h_kv, w.head_dim, lengths, block_size=w.block_size, table=table,
-                            num_splits=args.splits)
+                            num_splits=args.splits, remote=remote)
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
     stream = torch.cuda.current_stream()
     print(f"[bench] {w.name}: {len(lengths)} chunks, splits per chunk {runner.splits}", file=sys.stderr,
@@ -175,6 +185,7 @@ def main():
             "seq_len": w.seq_len, "chunks": n_chunks, "chunking": w.chunking,
             "block_size": w.block_size, "block_table": "permuted" if w.permuted else "identity",
             "split_plan": runner.splits,
+            "remote_kv": list(runner.remote) if runner.remote else None,
             "parallelism": "single GPU",
         },
         "pct_of_bf16_peak": round(100.0 * value / MFMA_BF16_PEAK_TFLOPS, 2),

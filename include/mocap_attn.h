@@ -157,6 +157,67 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
                               void* stream);
 
 /*
+ * mocap_chunk_attn_two_store -- mocap_chunk_attn for a chunk whose prefix KV
+ * lives partly in a second store: the memory-balanced KV reallocation of
+ * Section 4.1, where a debtor stage's KV accesses split into a remote portion
+ * (held by its paired creditor stage) and a local portion, combined here by
+ * the log-sum-exp merge of the split ranges.
+ *
+ *   kv, block_table, n_table   the first ("local") store: it holds positions
+ *               [0, remote_begin) and [remote_end, prefix_len + chunk_len),
+ *               including the chunk's own KV; n_table >=
+ *               ceil((prefix_len + chunk_len) / block_size)
+ *   remote_kv, remote_table, n_remote_table   the second ("remote") store: it
+ *               holds positions [remote_begin, remote_end); the same h_kv,
+ *               head_dim and block_size as kv; its table is indexed by the
+ *               same logical block numbers (position p in logical block
+ *               p / block_size), so n_remote_table >= ceil(remote_end /
+ *               block_size); only entries of blocks that overlap the range
+ *               are read.  Its pools may be any memory the device can read
+ *               (a peer device's HBM included).
+ *   remote_begin, remote_end   multiples of 64 with 0 <= remote_begin <=
+ *               remote_end <= prefix_len.  An empty range makes the call
+ *               identical to mocap_chunk_attn (remote arguments unused, may
+ *               be NULL).
+ *   num_splits  total number of KV ranges, or 0 to let the library choose;
+ *               raised to at least one prefix range per non-empty segment
+ *               ([0, remote_begin), the remote range, [remote_end,
+ *               prefix_len)) plus the chunk's own range, and clamped to what
+ *               the prefix allows.  Prefix ranges are shared out among the
+ *               segments in proportion to their lengths.
+ *   other arguments as in mocap_chunk_attn; the workspace must hold
+ *   mocap_chunk_attn_two_store_workspace_size bytes.
+ *
+ * Each store is read only at the positions it holds, so the other store's
+ * slots at those positions may hold anything (NaN included).  Results equal
+ * mocap_chunk_attn's within the tolerance of a split; they are bitwise equal
+ * to a single-store call whose split plan has the same range edges.
+ * Errors: as mocap_chunk_attn, plus INVALID_ARG for a malformed remote range,
+ * a remote store that differs in h_kv, head_dim or block_size, or a remote
+ * table that is too short or null.
+ */
+mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                                        const mocap_kv_store* remote_kv, const int32_t* remote_table,
+                                        int32_t n_remote_table, int64_t remote_begin, int64_t remote_end,
+                                        const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                        int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                                        void* workspace, size_t workspace_bytes, int32_t num_splits,
+                                        void* stream);
+
+/*
+ * mocap_chunk_attn_two_store_workspace_size -- the range count and workspace
+ * bytes of mocap_chunk_attn_two_store for the same shape, remote range and
+ * num_splits (see above).  splits_out may be NULL.
+ * Errors: INVALID_ARG for a null bytes_out, malformed sizes or remote range;
+ * UNSUPPORTED for head_dim not in {64, 128}; HIP if the device query fails
+ * (num_splits = 0 only).
+ */
+mocap_status mocap_chunk_attn_two_store_workspace_size(int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                                       int32_t h_kv, int32_t head_dim, int64_t remote_begin,
+                                                       int64_t remote_end, int32_t num_splits,
+                                                       int32_t* splits_out, size_t* bytes_out);
+
+/*
  * mocap_chunk_plan -- chunk lengths for a prompt of seq_len tokens (host only,
  * no device work).
  *

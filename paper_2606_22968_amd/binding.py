@@ -26,6 +26,8 @@ EXPORTED = (
     "mocap_kv_append",
     "mocap_chunk_attn_workspace_size",
     "mocap_chunk_attn",
+    "mocap_chunk_attn_two_store",
+    "mocap_chunk_attn_two_store_workspace_size",
     "mocap_chunk_plan",
     "mocap_lbcp_plan",
     "mocap_status_string",
@@ -79,6 +81,17 @@ def load_library():
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
         ctypes.c_int32, ctypes.c_void_p]
+    lib.mocap_chunk_attn_two_store.restype = st
+    lib.mocap_chunk_attn_two_store.argtypes = [
+        ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32,
+        ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+        ctypes.c_int32, ctypes.c_void_p]
+    lib.mocap_chunk_attn_two_store_workspace_size.restype = st
+    lib.mocap_chunk_attn_two_store_workspace_size.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+        ctypes.c_int64, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
     lib.mocap_lbcp_plan.restype = st
     lib.mocap_lbcp_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
@@ -188,6 +201,49 @@ def mocap_chunk_attn(store: KvStore, block_table: torch.Tensor, q: torch.Tensor,
         int(prefix_len), chunk_len, h_q, store.h_kv, head_dim, float(scale), o.data_ptr(),
         lse.data_ptr(), ws_ptr, ws_bytes, int(num_splits), _stream_handle(stream)),
         "mocap_chunk_attn")
+
+
+def mocap_chunk_attn_two_store_workspace_size(prefix_len: int, chunk_len: int, h_q: int, h_kv: int,
+                                              head_dim: int, remote_begin: int, remote_end: int,
+                                              num_splits: int = 0) -> Tuple[int, int]:
+    """Returns (number of KV ranges, workspace bytes)."""
+    splits = ctypes.c_int32(0)
+    nbytes = ctypes.c_size_t(0)
+    _check(load_library().mocap_chunk_attn_two_store_workspace_size(
+        int(prefix_len), int(chunk_len), int(h_q), int(h_kv), int(head_dim), int(remote_begin),
+        int(remote_end), int(num_splits), ctypes.byref(splits), ctypes.byref(nbytes)),
+        "mocap_chunk_attn_two_store_workspace_size")
+    return splits.value, nbytes.value
+
+
+def mocap_chunk_attn_two_store(store: KvStore, block_table: torch.Tensor, remote: Optional[KvStore],
+                               remote_table: Optional[torch.Tensor], remote_begin: int, remote_end: int,
+                               q: torch.Tensor, prefix_len: int, scale: float, o: torch.Tensor,
+                               lse: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+                               num_splits: int = 0, stream=None) -> None:
+    """As mocap_chunk_attn, with keys [remote_begin, remote_end) read from `remote`."""
+    _require(block_table, torch.int32, "block_table", 1)
+    _require(q, torch.bfloat16, "q", 3)
+    _require(o, torch.bfloat16, "o", 3)
+    _require(lse, torch.float32, "lse", 2)
+    chunk_len, h_q, head_dim = q.shape
+    if o.shape != q.shape or tuple(lse.shape) != (h_q, chunk_len):
+        raise ValueError("o must match q and lse must be [h_q][chunk_len]")
+    r_desc, r_table, r_n = None, None, 0
+    if remote is not None:
+        _require(remote_table, torch.int32, "remote_table", 1)
+        r_desc = ctypes.byref(remote.descriptor())
+        r_table, r_n = remote_table.data_ptr(), remote_table.numel()
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _require(workspace, workspace.dtype, "workspace")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    desc = store.descriptor()
+    _check(load_library().mocap_chunk_attn_two_store(
+        ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), r_desc, r_table, r_n,
+        int(remote_begin), int(remote_end), q.data_ptr(), int(prefix_len), chunk_len, h_q, store.h_kv,
+        head_dim, float(scale), o.data_ptr(), lse.data_ptr(), ws_ptr, ws_bytes, int(num_splits),
+        _stream_handle(stream)), "mocap_chunk_attn_two_store")
 
 
 def mocap_chunk_plan(seq_len: int, num_chunks: int, align: int = 128, balanced: bool = False) -> List[int]:

@@ -57,6 +57,11 @@ struct Plan {
   int64_t prefix_tiles;
   int n_ranges;
   size_t ws_bytes;
+  // Prefix tiles [remote_begin, remote_end) come from a second store; the
+  // prefix ranges are parts_before over [0, remote_begin), parts_remote over
+  // the second store's tiles and the rest over [remote_end, prefix_tiles).
+  int64_t remote_begin = 0, remote_end = 0;
+  int parts_before = 0, parts_remote = 0;
 };
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -199,6 +204,44 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
   return MOCAP_OK;
 }
 
+// Plan of a chunk whose prefix keys [64 tb, 64 te) live in a second store
+// (tb < te): the plan of make_plan for the same shape, with at least one
+// prefix range per non-empty segment (before, second store, after).  The
+// prefix ranges are shared out one by one to the segment with the most tiles
+// per range, never more ranges than tiles in a segment.
+mocap_status make_two_store_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
+                                 int32_t head_dim, int32_t num_splits, int64_t tb, int64_t te, Plan* plan) {
+  mocap_status st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, plan);
+  if (st != MOCAP_OK) return st;
+  const int64_t tiles[3] = {tb, te - tb, plan->prefix_tiles - te};
+  int parts[3] = {0, 0, 0};
+  int64_t wanted = plan->n_ranges - 1, segments = 0;
+  for (int i = 0; i < 3; ++i) {
+    if (tiles[i] > 0) {
+      parts[i] = 1;
+      ++segments;
+    }
+  }
+  wanted = std::min<int64_t>(std::max<int64_t>(wanted, segments), plan->prefix_tiles);
+  for (int64_t given = segments; given < wanted; ++given) {
+    int best = -1;
+    for (int i = 0; i < 3; ++i) {
+      if (parts[i] == 0 || parts[i] >= tiles[i]) continue;
+      // tiles[i] / parts[i] > tiles[best] / parts[best], in integers
+      if (best < 0 || tiles[i] * parts[best] > tiles[best] * parts[i]) best = i;
+    }
+    if (best < 0) break;
+    ++parts[best];
+  }
+  plan->parts_before = parts[0];
+  plan->parts_remote = parts[1];
+  plan->remote_begin = tb;
+  plan->remote_end = te;
+  plan->n_ranges = parts[0] + parts[1] + parts[2] + 1;
+  plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
+  return MOCAP_OK;
+}
+
 mocap_status check_store(const mocap_kv_store* kv) {
   if (kv == nullptr) return MOCAP_ERR_INVALID_ARG;
   if (kv->num_blocks <= 0 || kv->block_size <= 0 || kv->h_kv <= 0 || kv->head_dim <= 0)
@@ -215,6 +258,95 @@ mocap_status check_positions(const mocap_kv_store* kv, int32_t n_table, int64_t 
   const int64_t end = start + len;
   const int64_t blocks_needed = (end + kv->block_size - 1) / kv->block_size;
   if (blocks_needed > n_table) return MOCAP_ERR_INVALID_ARG;
+  return MOCAP_OK;
+}
+
+// Checks shared by the attention entry points (first store, sizes, pointers).
+mocap_status check_attn_args(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table, const void* q,
+                             int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv, int32_t head_dim,
+                             float scale, const void* o, const float* lse, int32_t num_splits) {
+  mocap_status st = check_store(kv);
+  if (st != MOCAP_OK) return st;
+  if (h_q <= 0 || h_kv <= 0 || h_q % h_kv != 0 || h_kv != kv->h_kv || head_dim != kv->head_dim)
+    return MOCAP_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return MOCAP_ERR_INVALID_ARG;
+  if (num_splits < 0) return MOCAP_ERR_INVALID_ARG;
+  st = check_positions(kv, n_table, prefix_len, chunk_len);
+  if (st != MOCAP_OK) return st;
+  if (chunk_len == 0) return MOCAP_OK;
+  if (!kv->k_pool || !kv->v_pool || !block_table || !q || !o || !lse) return MOCAP_ERR_INVALID_ARG;
+  if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || !aligned16(block_table) || !aligned16(q) ||
+      !aligned16(o) || !aligned16(lse))
+    return MOCAP_ERR_INVALID_ARG;
+  return MOCAP_OK;
+}
+
+// A second store's key range: whole 64-key tiles inside the prefix.
+bool valid_remote_range(int64_t begin, int64_t end, int64_t prefix_len) {
+  return begin >= 0 && begin <= end && end <= prefix_len && begin % kTileKeys == 0 && end % kTileKeys == 0;
+}
+
+// Launches the attention kernel (and the merge when the plan is split).
+// Arguments have been validated; remote_kv is used only for the plan's
+// second-store ranges.
+mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_table, const mocap_kv_store* remote_kv,
+                               const int32_t* remote_table, const Plan& plan, const void* q, int64_t prefix_len,
+                               int32_t chunk_len, int32_t h_q, int32_t h_kv, int32_t head_dim, float scale,
+                               void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  const int64_t total = (int64_t)plan.base_wgs * plan.n_ranges;
+  if (total > 0x7fffffff) return MOCAP_ERR_UNSUPPORTED;
+  if (plan.n_ranges > 1) {
+    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < plan.ws_bytes)
+      return MOCAP_ERR_WORKSPACE;
+  }
+
+  mocap::AttnLaunch p;
+  p.q = static_cast<const uint16_t*>(q);
+  p.k_pool = static_cast<const uint16_t*>(kv->k_pool);
+  p.v_pool = static_cast<const uint16_t*>(kv->v_pool);
+  p.table = block_table;
+  p.k_pool_r = remote_kv ? static_cast<const uint16_t*>(remote_kv->k_pool) : nullptr;
+  p.v_pool_r = remote_kv ? static_cast<const uint16_t*>(remote_kv->v_pool) : nullptr;
+  p.table_r = remote_kv ? remote_table : nullptr;
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.prefix_len = (int32_t)prefix_len;
+  p.prefix_tiles = (int32_t)plan.prefix_tiles;
+  p.chunk_len = chunk_len;
+  p.h_q = h_q;
+  p.h_kv = h_kv;
+  p.group = h_q / h_kv;
+  p.heads_per_wg = plan.hp;
+  p.row_groups = plan.row_groups;
+  p.block_size = kv->block_size;
+  p.n_ranges = plan.n_ranges;
+  p.remote_begin = (int32_t)plan.remote_begin;
+  p.remote_end = (int32_t)plan.remote_end;
+  p.parts_before = plan.parts_before;
+  p.parts_remote = plan.parts_remote;
+  p.total_wgs = (int)total;
+  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  p.ws_o = nullptr;
+  p.ws_lse = nullptr;
+  if (plan.n_ranges > 1) {
+    const size_t rows = (size_t)plan.n_ranges * (size_t)h_q * (size_t)chunk_len;
+    p.ws_o = static_cast<float*>(workspace);
+    p.ws_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                        round_up(rows * (size_t)head_dim * sizeof(float), 256));
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (mocap::launch_chunk_attn(p, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
+  if (plan.n_ranges > 1) {
+    mocap::MergeLaunch m;
+    m.ws_o = p.ws_o;
+    m.ws_lse = p.ws_lse;
+    m.o = p.o;
+    m.lse = lse;
+    m.chunk_len = chunk_len;
+    m.h_q = h_q;
+    m.n_ranges = plan.n_ranges;
+    if (mocap::launch_lse_merge(m, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
+  }
   return MOCAP_OK;
 }
 
@@ -287,71 +419,79 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
                               int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
                               void* workspace, size_t workspace_bytes, int32_t num_splits,
                               void* stream) {
-  mocap_status st = check_store(kv);
-  if (st != MOCAP_OK) return st;
-  if (h_q <= 0 || h_kv <= 0 || h_q % h_kv != 0 || h_kv != kv->h_kv || head_dim != kv->head_dim)
-    return MOCAP_ERR_INVALID_ARG;
-  if (!(scale > 0.f) || !std::isfinite(scale)) return MOCAP_ERR_INVALID_ARG;
-  if (num_splits < 0) return MOCAP_ERR_INVALID_ARG;
-  st = check_positions(kv, n_table, prefix_len, chunk_len);
-  if (st != MOCAP_OK) return st;
-  if (chunk_len == 0) return MOCAP_OK;
-  if (!kv->k_pool || !kv->v_pool || !block_table || !q || !o || !lse) return MOCAP_ERR_INVALID_ARG;
-  if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || !aligned16(block_table) || !aligned16(q) ||
-      !aligned16(o) || !aligned16(lse))
-    return MOCAP_ERR_INVALID_ARG;
-
+  mocap_status st = check_attn_args(kv, block_table, n_table, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
+                                    scale, o, lse, num_splits);
+  if (st != MOCAP_OK || chunk_len == 0) return st;
   Plan plan;
   st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
   if (st != MOCAP_OK) return st;
-  const int64_t total = (int64_t)plan.base_wgs * plan.n_ranges;
-  if (total > 0x7fffffff) return MOCAP_ERR_UNSUPPORTED;
-  if (plan.n_ranges > 1) {
-    if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < plan.ws_bytes)
-      return MOCAP_ERR_WORKSPACE;
-  }
+  return enqueue_attention(kv, block_table, nullptr, nullptr, plan, q, prefix_len, chunk_len, h_q, h_kv,
+                           head_dim, scale, o, lse, workspace, workspace_bytes, stream);
+}
 
-  mocap::AttnLaunch p;
-  p.q = static_cast<const uint16_t*>(q);
-  p.k_pool = static_cast<const uint16_t*>(kv->k_pool);
-  p.v_pool = static_cast<const uint16_t*>(kv->v_pool);
-  p.table = block_table;
-  p.o = static_cast<uint16_t*>(o);
-  p.lse = lse;
-  p.prefix_len = (int32_t)prefix_len;
-  p.prefix_tiles = (int32_t)plan.prefix_tiles;
-  p.chunk_len = chunk_len;
-  p.h_q = h_q;
-  p.h_kv = h_kv;
-  p.group = h_q / h_kv;
-  p.heads_per_wg = plan.hp;
-  p.row_groups = plan.row_groups;
-  p.block_size = kv->block_size;
-  p.n_ranges = plan.n_ranges;
-  p.total_wgs = (int)total;
-  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  p.ws_o = nullptr;
-  p.ws_lse = nullptr;
-  if (plan.n_ranges > 1) {
-    const size_t rows = (size_t)plan.n_ranges * (size_t)h_q * (size_t)chunk_len;
-    p.ws_o = static_cast<float*>(workspace);
-    p.ws_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                        round_up(rows * (size_t)head_dim * sizeof(float), 256));
+mocap_status mocap_chunk_attn_two_store_workspace_size(int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                                       int32_t h_kv, int32_t head_dim, int64_t remote_begin,
+                                                       int64_t remote_end, int32_t num_splits,
+                                                       int32_t* splits_out, size_t* bytes_out) {
+  if (bytes_out == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (prefix_len < 0 || chunk_len < 0 || h_q <= 0 || h_kv <= 0 || h_q % h_kv != 0 || num_splits < 0)
+    return MOCAP_ERR_INVALID_ARG;
+  if (prefix_len + (int64_t)chunk_len > kMaxPositions) return MOCAP_ERR_INVALID_ARG;
+  if (!supported_head_dim(head_dim)) return MOCAP_ERR_UNSUPPORTED;
+  if (!valid_remote_range(remote_begin, remote_end, prefix_len)) return MOCAP_ERR_INVALID_ARG;
+  if (chunk_len == 0) {
+    if (splits_out) *splits_out = 1;
+    *bytes_out = 0;
+    return MOCAP_OK;
   }
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (mocap::launch_chunk_attn(p, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
-  if (plan.n_ranges > 1) {
-    mocap::MergeLaunch m;
-    m.ws_o = p.ws_o;
-    m.ws_lse = p.ws_lse;
-    m.o = p.o;
-    m.lse = lse;
-    m.chunk_len = chunk_len;
-    m.h_q = h_q;
-    m.n_ranges = plan.n_ranges;
-    if (mocap::launch_lse_merge(m, head_dim, s) != hipSuccess) return MOCAP_ERR_HIP;
-  }
+  Plan plan;
+  const mocap_status st =
+      remote_begin == remote_end
+          ? make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan)
+          : make_two_store_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits,
+                                remote_begin / kTileKeys, remote_end / kTileKeys, &plan);
+  if (st != MOCAP_OK) return st;
+  if (splits_out) *splits_out = plan.n_ranges;
+  *bytes_out = plan.ws_bytes;
   return MOCAP_OK;
+}
+
+mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                                        const mocap_kv_store* remote_kv, const int32_t* remote_table,
+                                        int32_t n_remote_table, int64_t remote_begin, int64_t remote_end,
+                                        const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                        int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                                        void* workspace, size_t workspace_bytes, int32_t num_splits,
+                                        void* stream) {
+  mocap_status st = check_attn_args(kv, block_table, n_table, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
+                                    scale, o, lse, num_splits);
+  if (st != MOCAP_OK) return st;
+  if (!valid_remote_range(remote_begin, remote_end, prefix_len)) return MOCAP_ERR_INVALID_ARG;
+  if (remote_begin == remote_end) {
+    if (chunk_len == 0) return MOCAP_OK;
+    Plan plan;
+    st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
+    if (st != MOCAP_OK) return st;
+    return enqueue_attention(kv, block_table, nullptr, nullptr, plan, q, prefix_len, chunk_len, h_q, h_kv,
+                             head_dim, scale, o, lse, workspace, workspace_bytes, stream);
+  }
+  st = check_store(remote_kv);
+  if (st != MOCAP_OK) return st;
+  if (remote_kv->h_kv != kv->h_kv || remote_kv->head_dim != kv->head_dim ||
+      remote_kv->block_size != kv->block_size)
+    return MOCAP_ERR_INVALID_ARG;
+  st = check_positions(remote_kv, n_remote_table, 0, (int32_t)remote_end);
+  if (st != MOCAP_OK) return st;
+  if (chunk_len == 0) return MOCAP_OK;
+  if (!remote_kv->k_pool || !remote_kv->v_pool || !remote_table || !aligned16(remote_kv->k_pool) ||
+      !aligned16(remote_kv->v_pool) || !aligned16(remote_table))
+    return MOCAP_ERR_INVALID_ARG;
+  Plan plan;
+  st = make_two_store_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, remote_begin / kTileKeys,
+                           remote_end / kTileKeys, &plan);
+  if (st != MOCAP_OK) return st;
+  return enqueue_attention(kv, block_table, remote_kv, remote_table, plan, q, prefix_len, chunk_len, h_q, h_kv,
+                           head_dim, scale, o, lse, workspace, workspace_bytes, stream);
 }
 
 mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align, int32_t balanced,

@@ -17,11 +17,22 @@ constexpr int kGroupThreads = 64 * kWavesPerGroup;
 // One launch of the attention kernel: every workgroup owns `heads_per_wg`
 // query heads of one GQA group times `32 * 8 / heads_per_wg` query rows, for
 // one KV range.
+//
+// KV ranges, in order: `parts_before` ranges cutting tiles [0, remote_begin)
+// (first store), `parts_remote` ranges cutting tiles [remote_begin,
+// remote_end) (second store), the remaining n_ranges - 1 - parts_before -
+// parts_remote ranges cutting tiles [remote_end, ceil(P / 64)) (first store;
+// the last one ends at P), then the chunk's own keys [P, P + L) (first
+// store).  Tile t holds keys [64 t, 64 t + 64).  n_ranges == 1 is the
+// unsplit launch over [0, P + L) from the first store.
 struct AttnLaunch {
   const uint16_t* q;        // bf16 [L][Hq][D]
   const uint16_t* k_pool;   // bf16 [nb][Hkv][bs][D]
   const uint16_t* v_pool;   // bf16 [nb][Hkv][D][bs]
   const int32_t* table;     // logical block -> physical block
+  const uint16_t* k_pool_r; // second store (same layout and block size), or null
+  const uint16_t* v_pool_r;
+  const int32_t* table_r;
   uint16_t* o;              // bf16 [L][Hq][D]         (unsplit)
   float* lse;               // fp32 [Hq][L]            (unsplit)
   float* ws_o;              // fp32 [R][Hq][L][D]      (split partials)
@@ -36,6 +47,10 @@ struct AttnLaunch {
   int32_t row_groups;       // ceil(L / rows_per_wg)
   int32_t block_size;
   int32_t n_ranges;         // 1 = unsplit; else prefix ranges + 1 chunk range
+  int32_t remote_begin;     // tiles [remote_begin, remote_end) live in the second store
+  int32_t remote_end;
+  int32_t parts_before;     // ranges over tiles [0, remote_begin)
+  int32_t parts_remote;     // ranges over the second store's tiles
   int32_t total_wgs;
   float scale_log2;         // scale * log2(e)
 };

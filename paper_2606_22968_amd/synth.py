@@ -66,6 +66,15 @@ def make_qkv(seed: int, seq_len: int, h_q: int, h_kv: int, head_dim: int):
     return q, k, v
 
 
+def prefixes(lengths) -> List[int]:
+    """P_c of every chunk: the number of tokens before it."""
+    out, acc = [], 0
+    for n in lengths:
+        out.append(acc)
+        acc += n
+    return out
+
+
 def identity_table(num_blocks: int) -> torch.Tensor:
     return torch.arange(num_blocks, dtype=torch.int32)
 

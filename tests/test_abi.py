@@ -142,3 +142,67 @@ def test_workspace_size_forced_splits(mocap_lib):
         ws(4096, 256, 32, 8, 96, 1)
     with pytest.raises(mocap_lib.MocapError):
         ws(4096, 256, 30, 8, 128, 1)
+
+
+def attn2(mocap_lib, kv=None, table=FAKE, n_table=64, rkv=None, rtable=FAKE, n_rtable=64, rb=0, re=512,
+          q=FAKE, P=1024, L=256, h_q=32, h_kv=8, d=128, scale=0.088, o=FAKE, lse=FAKE, ws=None, ws_bytes=0,
+          splits=2):
+    lib = mocap_lib.load_library()
+    kv = store(mocap_lib) if kv is None else kv
+    rkv = store(mocap_lib) if rkv is None else rkv
+    rref = ctypes.byref(rkv) if rkv != "null" else None
+    return lib.mocap_chunk_attn_two_store(ctypes.byref(kv), table, n_table, rref, rtable, n_rtable, rb, re, q,
+                                          P, L, h_q, h_kv, d, scale, o, lse, ws, ws_bytes, splits, None)
+
+
+@pytest.mark.parametrize("kwargs,expect", [
+    (dict(rb=-64), INVALID),
+    (dict(rb=512, re=256), INVALID),               # begin after end
+    (dict(re=1088), INVALID),                      # beyond the prefix
+    (dict(re=500), INVALID),                       # not a whole tile
+    (dict(rb=32), INVALID),
+    (dict(rkv="null"), INVALID),
+    (dict(rtable=0), INVALID),
+    (dict(rtable=MIS), INVALID),
+    (dict(n_rtable=1), INVALID),                   # 512 positions need 2 blocks
+    (dict(rkv="h_kv"), INVALID),
+    (dict(rkv="block"), INVALID),
+    (dict(rkv="dim"), INVALID),
+    (dict(scale=0.0), INVALID),
+    (dict(n_table=4), INVALID),
+    (dict(splits=1), WORKSPACE),                   # a remote range always splits
+])
+def test_two_store_rejects(mocap_lib, kwargs, expect):
+    variants = {"h_kv": dict(h_kv=4), "block": dict(block_size=128), "dim": dict(head_dim=64)}
+    if kwargs.get("rkv") in variants:
+        kwargs = dict(kwargs, rkv=store(mocap_lib, **variants[kwargs["rkv"]]))
+    assert attn2(mocap_lib, **kwargs) == expect
+
+
+def test_two_store_empty_remote_range_is_single_store(mocap_lib):
+    # remote arguments unused: the same status as mocap_chunk_attn
+    assert attn2(mocap_lib, rkv="null", rtable=0, n_rtable=0, rb=256, re=256, splits=3) == WORKSPACE
+    assert attn2(mocap_lib, rkv="null", rtable=0, n_rtable=0, rb=0, re=0, L=0, q=0, o=0, lse=0) == 0
+
+
+def test_two_store_workspace_size(mocap_lib):
+    ws2 = mocap_lib.mocap_chunk_attn_two_store_workspace_size
+    ws = mocap_lib.mocap_chunk_attn_workspace_size
+
+    def nbytes(r):
+        rows = r * 32 * 256
+        return rows * 128 * 4 + rows * 4
+
+    # P = 4096 (64 tiles), L = 256.  Remote in the middle: three segments.
+    assert ws2(4096, 256, 32, 8, 128, 1024, 2048, 1) == (4, nbytes(4))   # raised to 3 + 1
+    assert ws2(4096, 256, 32, 8, 128, 1024, 2048, 10) == (10, nbytes(10))
+    assert ws2(4096, 256, 32, 8, 128, 0, 2048, 1) == (3, nbytes(3))      # remote first
+    assert ws2(4096, 256, 32, 8, 128, 2048, 4096, 2) == (3, nbytes(3))   # remote last
+    assert ws2(4096, 256, 32, 8, 128, 0, 4096, 1) == (2, nbytes(2))      # all remote
+    assert ws2(4096, 256, 32, 8, 128, 0, 4096, 500)[0] == 65             # one range per tile at most
+    assert ws2(4096, 256, 32, 8, 128, 1024, 1024, 5) == ws(4096, 256, 32, 8, 128, 5)
+    assert ws2(4096, 0, 32, 8, 128, 0, 1024, 0) == (1, 0)
+    for bad in [(4096, 256, 32, 8, 128, 0, 4097, 0), (4096, 256, 32, 8, 128, 64, 0, 0),
+                (4096, 256, 32, 8, 128, 10, 64, 0)]:
+        with pytest.raises(mocap_lib.MocapError):
+            ws2(*bad)
