@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const int fast_end = max(fast_begin, min(tile_end, min(hi, P + wg_row0 + 1) / kTileKeys));
   const int n_fast = fast_end - fast_begin;
   const int n_tiles = tile_end - tile_begin;
-  auto seq_tile = [&](int i) -> int {
+  auto seq_tile = [&](int i) __attribute__((always_inline)) -> int {
     if (i < n_fast) return fast_begin + i;
     if (i < n_fast + n_head) return tile_begin;
     return fast_end + (i - n_fast - n_head);
@@ -250,7 +250,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ v_swizzle(vr);
     v_src[j] = vr * p.block_size + vc * 8;
   }
-  auto issue_seq = [&](int i) {
+  auto issue_seq = [&](int i) __attribute__((always_inline)) {
     const int t = seq_tile(i);
     const int pos0 = t * kTileKeys;
     const int lb = pos0 / p.block_size;
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       __builtin_amdgcn_global_load_lds(vb + v_src[j], (lds_ptr_t)(vl + dst), 16, 0, 0);
     }
   };
-  auto publish_seq = [&](int i, int later) {
+  auto publish_seq = [&](int i, int later) __attribute__((always_inline)) {
     if (later >= 2) {
       wait_vmem<2 * TILE_OPS>();
     } else if (later == 1) {
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const int v_row_sw = v_swizzle(l32);
   const uint32_t ones = 0x3F803F80u;
 
-  auto visible_bits = [&](int base) -> uint32_t {
+  auto visible_bits = [&](int base) __attribute__((always_inline)) -> uint32_t {
     const int a = lo - base;
     const int b = min(hi, P + row0 + l32 + 1) - base;
     auto first_i = [](int x) { return x <= 0 ? 0 : x <= 8 ? x : x <= 16 ? 8 : x <= 24 ? x - 8 : 16; };
@@ -310,16 +310,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // 32-key half (VALU), settle, P*V (16 MFMAs).
   f32x16 s[2];
   uint32_t vis[2] = {0xFFFFu, 0xFFFFu};
-  uint32_t pk[2][8];
+  uint32_t pk[2][2][8];  // [buffer][32-key half][packed pairs]: tile i uses buffer i % 2
   float rs[2];
-  auto scores = [&](int i, bool masked) {
+  auto scores = [&](int i, bool masked) __attribute__((always_inline)) {
     const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     const uint16_t* krow0 = kl + k_row_lo * D;
     const uint16_t* krow1 = kl + (32 + k_row_lo) * D;
     const int ksw0 = k_swizzle<D>(k_row_lo), ksw1 = k_swizzle<D>(32 + k_row_lo);
     // The two 32-key halves are independent accumulation chains; their K
     // fragments are read two k-steps ahead of the MFMAs that use them.
-    auto kfrag = [&](const uint16_t* krow, int ksw, int ks) {
+    auto kfrag = [&](const uint16_t* krow, int ksw, int ks) __attribute__((always_inline)) {
       return *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
     };
     bf16x8 a0[KS], a1[KS];
@@ -344,37 +344,56 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       vis[1] = visible_bits(tstart + 32 + half * 8);
     }
   };
-  auto probs_half = [&](int sb, bool masked) {
-    const float neg_m = -m_run;
+  // Probabilities of both 32-key halves into buffer b: exponentials and
+  // packing first (one straight run of VALU work), then the mask of a
+  // straddling tile, then the row sums.
+  auto probs = [&](int b, bool masked, float neg_m) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i2 = 0; i2 < 16; i2 += 2) {
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, neg_m));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
-      pk[sb][i2 / 2] = pack_bf16x2(e0, e1);
-    }
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int i2 = 0; i2 < 16; i2 += 2) {
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, neg_m));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
+        pk[b][sb][i2 / 2] = pack_bf16x2(e0, e1);
+      }
     if (masked) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[sb], 2 * j, 1);
-        const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vis[sb], 2 * j + 1, 1);
-        pk[sb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
+      for (int sb = 0; sb < 2; ++sb) {
+        uint32_t vm = vis[sb];
+        asm volatile("" : "+v"(vm));  // keeps the per-pair masks from being computed early
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vm, 2 * j, 1);
+          const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vm, 2 * j + 1, 1);
+          pk[b][sb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
+        }
       }
     }
-    float acc = 0.f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[sb][j], ones, acc);
-    rs[sb] = acc;
+    for (int sb = 0; sb < 2; ++sb) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[b][sb][j], ones, acc);
+      rs[sb] = acc;
+    }
   };
-  auto settle = [&]() {
+  auto settle = [&](int b) __attribute__((always_inline)) {
     const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
       const bool row_over = lane_pair_max(over ? 1.f : 0.f) > 0.f;
+      // The visibility masks pass through an empty asm statement here, so the
+      // compiler cannot hoist this rare path's per-element bit selects into
+      // the main loop (where they would hold registers).
+      asm volatile("" : "+v"(vis[0]), "+v"(vis[1]));
+      // Largest visible score of the block: invisible ones read as -inf.
       float mx = -INFINITY;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int i2 = 0; i2 < 16; ++i2)
-          if ((vis[sb] >> i2) & 1u) mx = fmaxf(mx, s[sb][i2]);
+        for (int i2 = 0; i2 < 16; ++i2) {
+          const int keep = __builtin_amdgcn_sbfe((int)vis[sb], i2, 1);
+          mx = fmaxf(mx, __int_as_float((__float_as_int(s[sb][i2]) & keep) | (~keep & (int)0xFF800000u)));
+        }
       mx = lane_pair_max(mx) * sl2;
       const bool fresh = lane_pair_sum(l_run) == 0.f;
       if (row_over && !fresh) {
@@ -384,84 +403,71 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       if (row_over && fresh) {
         m_run = mx;
         const float nm = m_run == -INFINITY ? 0.f : -m_run;
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb) {
-          float acc = 0.f;
-#pragma unroll
-          for (int i2 = 0; i2 < 16; i2 += 2) {
-            const float e0 = ((vis[sb] >> i2) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, nm)) : 0.f;
-            const float e1 = ((vis[sb] >> (i2 + 1)) & 1u) ? __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, nm)) : 0.f;
-            pk[sb][i2 / 2] = pack_bf16x2(e0, e1);
-            acc = dot2_bf16(pk[sb][i2 / 2], ones, acc);
-          }
-          rs[sb] = acc;
-        }
+        probs(b, true, nm);
       }
     }
     l_run += rs[0] + rs[1];
   };
-  auto pv = [&](int i) {
+  auto pv = [&](int i, int b) __attribute__((always_inline)) {
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
-    auto vfrag = [&](int kst, int md) {
+    auto vfrag = [&](int kst, int md) __attribute__((always_inline)) {
       const int vchunk = (kst * 2 + half) ^ v_row_sw;
       return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
     };
-    // V fragments of the next 16-key step are read while the current step's
-    // four (independent) MFMAs run.
-    bf16x8 vf[4][MD];
-#pragma unroll
-    for (int md = 0; md < MD; ++md) vf[0][md] = vfrag(0, md);
 #pragma unroll
     for (int kst = 0; kst < 4; ++kst) {
-      if (kst + 1 < 4) {
-#pragma unroll
-        for (int md = 0; md < MD; ++md) vf[kst + 1][md] = vfrag(kst + 1, md);
-      }
       const int sb = kst / 2, kk = kst % 2;
       const bf16x8 pb = __builtin_bit_cast(
-          bf16x8, u32x4{pk[sb][kk * 4], pk[sb][kk * 4 + 1], pk[sb][kk * 4 + 2], pk[sb][kk * 4 + 3]});
+          bf16x8, u32x4{pk[b][sb][kk * 4], pk[b][sb][kk * 4 + 1], pk[b][sb][kk * 4 + 2], pk[b][sb][kk * 4 + 3]});
 #pragma unroll
       for (int md = 0; md < MD; ++md)
-        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kst][md], pb, oacc[md], 0, 0, 0);
+        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kst, md), pb, oacc[md], 0, 0, 0);
     }
   };
   // Barrier k publishes tile k and frees the stage of tile k-2, which tile
-  // k+2 refills.  Group A (waves 0-3) meets barrier k before its scores of
-  // tile k; group B (waves 4-7) meets it between the two probability halves
-  // of tile k-1, so B runs one phase behind A and the two waves sharing a
-  // SIMD alternate between MFMA and VALU work.
-  auto barrier_k = [&](int k) {
+  // k+2 refills.  Every wave meets it at the top of tile k.
+  auto barrier_k = [&](int k) __attribute__((always_inline)) {
     publish_seq(k, min(n_tiles - 1 - k, 1));
     if (k + 2 < n_tiles) issue_seq(k + 2);
   };
-  const bool group_b = wave >= 4;
+  // Tile i: scores, then the previous tile's P*V (MFMA) in the same basic
+  // block as this tile's probabilities (VALU), so one wave keeps both the
+  // matrix and the vector units busy; the probabilities alternate between
+  // two buffers.  Tile 0 has no predecessor.
+  auto first_tile = [&](bool masked) __attribute__((always_inline)) {
+    barrier_k(0);
+    scores(0, masked);
+    probs(0, masked, -m_run);
+    settle(0);
+  };
+  auto next_tile = [&](int i, int b, bool masked) __attribute__((always_inline)) {
+    barrier_k(i);
+    scores(i, masked);
+    pv(i - 1, b ^ 1);
+    probs(b, masked, -m_run);
+    settle(b);
+  };
 
   for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
     if (tid == 0) rerun_flag = 0;
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
-    if (!group_b) {
-      for (int i = 0; i < n_tiles; ++i) {
-        const bool masked = i >= n_fast;
-        barrier_k(i);
-        scores(i, masked);
-        probs_half(0, masked);
-        probs_half(1, masked);
-        settle();
-        pv(i);
-      }
+    if (n_fast > 0) {
+      first_tile(false);
     } else {
-      barrier_k(0);
-      for (int i = 0; i < n_tiles; ++i) {
-        const bool masked = i >= n_fast;
-        scores(i, masked);
-        probs_half(0, masked);
-        if (i + 1 < n_tiles) barrier_k(i + 1);
-        probs_half(1, masked);
-        settle();
-        pv(i);
-      }
+      first_tile(true);
     }
+    for (int i = 1; i < n_tiles; i += 2) {
+      next_tile(i, 1, i >= n_fast);
+      if (i + 1 < n_tiles) next_tile(i + 1, 0, i + 1 >= n_fast);
+    }
+    if ((n_tiles - 1) & 1) {  // the last tile's probabilities are in buffer 1
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
+    }
+    pv(n_tiles - 1, 0);
     if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(&rerun_flag, 1);
     lds_barrier();
     const bool again = rerun_flag != 0;
