@@ -13,10 +13,10 @@
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
 //     (global_load_lds_dwordx4, no staging registers) into a 4-stage ring,
 //     prefetched two tiles ahead, one workgroup barrier per tile.
-//   * Ping-pong: waves 0-3 meet the barrier of tile k before their scores of
-//     tile k, waves 4-7 in the middle of their softmax of tile k-1, so the two
-//     waves on each SIMD stay half a tile apart and one's exp/pack VALU work
-//     overlaps the other's MFMAs.
+//   * Software pipelining inside each wavefront: tile k's scores are followed
+//     by tile k-1's P*V product and tile k's exp/pack work in one basic block,
+//     so the MFMAs of one tile and the VALU work of the next issue side by
+//     side.  The probabilities alternate between two register buffers.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane's accumulator then holds one query and
 //     16 keys, so row statistics need one cross-half exchange
