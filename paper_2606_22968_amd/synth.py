@@ -66,6 +66,20 @@ def make_qkv(seed: int, seq_len: int, h_q: int, h_kv: int, head_dim: int):
     return q, k, v
 
 
+def make_kv_long(seed: int, n_tokens: int, h_kv: int, head_dim: int, piece: int = 65536):
+    """K, V [n][Hkv][d] CPU bf16 for very long sequences, drawn N(0, 1) piece by
+    piece (each piece from its own seeded generator) to bound host memory."""
+    k = torch.empty((n_tokens, h_kv, head_dim), dtype=torch.bfloat16)
+    v = torch.empty((n_tokens, h_kv, head_dim), dtype=torch.bfloat16)
+    for i, start in enumerate(range(0, n_tokens, piece)):
+        n = min(piece, n_tokens - start)
+        g = torch.Generator(device="cpu")
+        g.manual_seed(seed * 100003 + i)
+        k[start:start + n] = torch.randn((n, h_kv, head_dim), generator=g, dtype=torch.float32).to(torch.bfloat16)
+        v[start:start + n] = torch.randn((n, h_kv, head_dim), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    return k, v
+
+
 def prefixes(lengths) -> List[int]:
     """P_c of every chunk: the number of tokens before it."""
     out, acc = [], 0
