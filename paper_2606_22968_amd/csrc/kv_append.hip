@@ -10,8 +10,9 @@
 // with phys = table[(P + t) / bs] and slot = (P + t) % bs.
 //
 // One workgroup moves 64 positions of one KV head.  K rows go straight out as
-// 16-byte stores.  V goes through LDS so that the transposed stores of a
-// wavefront cover consecutive slots of one head-dim row.
+// 16-byte stores.  V goes through LDS so that the transposed stores cover
+// consecutive slots of one head-dim row: 16 bytes per thread for a whole
+// 64-aligned tile, 2 bytes per lane at ragged edges.
 #include "internal.h"
 
 namespace mocap {
@@ -49,7 +50,24 @@ __global__ __launch_bounds__(kGroupThreads) void kv_append_kernel(const AppendLa
   }
   __syncthreads();
 
-  // Transposed V stores: lane -> position, wavefront -> head-dim rows.
+  const int64_t pos0 = p.start_pos + t0;
+  if (n_tok == kTileKeys && pos0 % kTileKeys == 0) {
+    // A whole aligned tile (one block holds it): each thread gathers 8
+    // consecutive positions of one head-dim row and stores them as 16 bytes.
+    const int64_t lb = pos0 / p.block_size;
+    const int64_t slot0 = pos0 - lb * p.block_size;
+    uint16_t* base = p.v_pool + ((int64_t)p.table[lb] * p.h_kv + h) * D * (int64_t)p.block_size + slot0;
+    for (int c = tid; c < D * (kTileKeys / 8); c += kGroupThreads) {
+      const int e = c / (kTileKeys / 8), g = c % (kTileKeys / 8);
+      u32x4 out;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        out[j] = (uint32_t)vt[(g * 8 + 2 * j) * PITCH + e] | ((uint32_t)vt[(g * 8 + 2 * j + 1) * PITCH + e] << 16);
+      *reinterpret_cast<u32x4*>(base + (int64_t)e * p.block_size + g * 8) = out;
+    }
+    return;
+  }
+  // Otherwise (ragged edges): lane -> position, wavefront -> head-dim rows.
   const int lane = tid & 63;
   const int wave = tid >> 6;
   if (lane < n_tok) {
