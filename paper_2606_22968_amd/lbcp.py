@@ -16,6 +16,10 @@ Run as a module to measure, fit, plan and compare against the closed-form
 balanced plan:
 
     python -m paper_2606_22968_amd.lbcp --workload llama8b_128k_balanced --stages 16
+
+With --layer, EvaluateChunk is the latency of a whole decoder layer per chunk
+(projections and feed-forward network included, layer.py), so both terms of
+Eq. (1) enter the model.
 """
 import argparse
 import json
@@ -113,15 +117,54 @@ def measure(h_q: int, h_kv: int, head_dim: int, plans: Sequence[Sequence[int]], 
     return out
 
 
+def measure_layer(shape, plans: Sequence[Sequence[int]], reps: int = 3, seed: int = 0, block_size: int = 256):
+    """As measure(), for a whole decoder layer per chunk (layer.ChunkedLayer):
+    returns [(plan_index, chunk_len, prefix_len, total_us, attention_us, gemm_us)],
+    attention_us covering mocap_kv_append + mocap_chunk_attn and gemm_us the
+    projections and the feed-forward network."""
+    import torch
+
+    from .layer import ChunkedLayer
+
+    seq_len = sum(plans[0])
+    if any(sum(p) != seq_len for p in plans):
+        raise ValueError("every plan must cover the same sequence")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    x = torch.randn((seq_len, shape.hidden), generator=g, dtype=torch.float32).to(torch.bfloat16).cuda()
+    scale = shape.head_dim ** -0.5
+    stream = torch.cuda.current_stream()
+    out = []
+    for i, lengths in enumerate(plans):
+        layer = ChunkedLayer(shape, lengths, seed=seed, block_size=block_size)
+        layer.run(x, scale, stream=stream)  # warm-up
+        ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in lengths] for _ in range(reps)]
+        for r in range(reps):
+            layer.run(x, scale, stream=stream, events=ev[r])
+        torch.cuda.synchronize()
+        for c, (n, p) in enumerate(zip(layer.lengths, layer.prefixes)):
+            def med(a, b):
+                return statistics.median(ev[r][c][a].elapsed_time(ev[r][c][b]) * 1e3 for r in range(reps))
+            total, attn = med(0, 3), med(1, 2)
+            out.append((i, n, p, total, attn, total - attn))
+        del layer
+    return out
+
+
 def _objective(latencies: Sequence[float], num_stages: int) -> float:
     return sum(latencies) + (num_stages - 1) * max(latencies)
 
 
 def main(argv=None):
     from . import synth
+    from .layer import SHAPES
 
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--workload", default="llama8b_128k_balanced")
+    ap.add_argument("--layer", choices=sorted(SHAPES), default=None,
+                    help="time a whole decoder layer per chunk (projections, attention, feed-forward) "
+                         "instead of the attention calls alone")
+    ap.add_argument("--seq-len", type=int, default=0, help="0 = the workload's sequence length")
     ap.add_argument("--stages", type=int, default=16, help="pipeline stages N of the objective")
     ap.add_argument("--chunks", type=int, default=0, help="0 = the workload's chunk count")
     ap.add_argument("--align", type=int, default=0, help="0 = the workload's alignment")
@@ -130,32 +173,42 @@ def main(argv=None):
     args = ap.parse_args(argv)
 
     w = synth.WORKLOADS[args.workload]
+    seq_len = args.seq_len or w.seq_len
     m = args.chunks or w.num_chunks
     align = args.align or w.align
-    probes = probe_plans(w.seq_len, m, align, seed=w.seed, n_random=args.random_plans)
-    print(f"[lbcp] measuring {len(probes)} probe plans of {w.name}", file=sys.stderr, flush=True)
-    samples = measure(w.h_q, w.h_kv, w.head_dim, probes, w.scale, w.block_size, args.reps, w.seed)
-    model = fit([(c, p, t) for _, c, p, t in samples])
-    dp_lengths, t_max, t_sum = plan(w.seq_len, m, args.stages, align, model)
+    probes = probe_plans(seq_len, m, align, seed=w.seed, n_random=args.random_plans)
+    shape = SHAPES[args.layer] if args.layer else None
+    what = f"{shape.name} decoder layer" if shape else f"{w.name} attention"
+
+    def timed(plans):
+        if shape is None:
+            return [(i, c, p, t, t, 0.0) for i, c, p, t in
+                    measure(w.h_q, w.h_kv, w.head_dim, plans, w.scale, w.block_size, args.reps, w.seed)]
+        return measure_layer(shape, plans, args.reps, w.seed, w.block_size)
+
+    print(f"[lbcp] measuring {len(probes)} probe plans of {what}, S={seq_len}", file=sys.stderr, flush=True)
+    samples = timed(probes)
+    model = fit([(c, p, t) for _, c, p, t, _, _ in samples])
+    dp_lengths, t_max, t_sum = plan(seq_len, m, args.stages, align, model)
     closed = probes[1]
     print("[lbcp] measuring the closed-form and dynamic-programming plans", file=sys.stderr, flush=True)
-    final = measure(w.h_q, w.h_kv, w.head_dim, [closed, dp_lengths], w.scale, w.block_size, args.reps, w.seed)
-    lat = {i: [t for j, _, _, t in final if j == i] for i in (0, 1)}
+    final = timed([closed, dp_lengths])
+
+    def summary(i, lengths):
+        rows = [x for x in final if x[0] == i]
+        lat = [x[3] for x in rows]
+        return {"lengths": list(lengths), "chunk_us": [round(t, 1) for t in lat],
+                "attention_us": [round(x[4], 1) for x in rows], "gemm_us": [round(x[5], 1) for x in rows],
+                "max_over_min": round(max(lat) / min(lat), 3),
+                "objective_us": round(_objective(lat, args.stages), 1)}
+
     report = {
-        "workload": w.name,
-        "stages": args.stages,
-        "chunks": m,
-        "align": align,
+        "workload": what, "seq_len": seq_len, "stages": args.stages, "chunks": m, "align": align,
         "model_us": {"cost_pair": model.cost_pair, "cost_token": model.cost_token,
                      "cost_chunk": model.cost_chunk, "rms_rel_err": round(model.rms_rel_err, 4),
                      "samples": len(samples)},
-        "closed_form": {"lengths": closed, "chunk_us": [round(t, 1) for t in lat[0]],
-                        "max_over_min": round(max(lat[0]) / min(lat[0]), 3),
-                        "objective_us": round(_objective(lat[0], args.stages), 1)},
-        "dp": {"lengths": dp_lengths, "chunk_us": [round(t, 1) for t in lat[1]],
-               "max_over_min": round(max(lat[1]) / min(lat[1]), 3),
-               "objective_us": round(_objective(lat[1], args.stages), 1),
-               "model_t_max_us": round(t_max, 1), "model_t_sum_us": round(t_sum, 1)},
+        "closed_form": summary(0, closed),
+        "dp": dict(summary(1, dp_lengths), model_t_max_us=round(t_max, 1), model_t_sum_us=round(t_sum, 1)),
     }
     print(json.dumps(report), flush=True)
     return report
