@@ -11,8 +11,11 @@
 //     share one KV head (GQA packing), so each K/V tile staged in LDS serves
 //     every query head of the group.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
-//     (global_load_lds_dwordx4, no staging registers) into a 4-stage ring,
-//     prefetched two tiles ahead, one workgroup barrier per tile.
+//     (global_load_lds_dwordx4, no staging registers) into a 5-stage ring
+//     (160 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
+//     barrier per tile.  Waves 4-7 meet each barrier after their scores, half
+//     a tile behind waves 0-3, so one wave's score MFMAs overlap the other's
+//     softmax on each SIMD.
 //   * Software pipelining inside each wavefront: tile k's scores are followed
 //     by tile k-1's P*V product and tile k's exp/pack work in one basic block,
 //     so the MFMAs of one tile and the VALU work of the next issue side by
@@ -163,10 +166,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   constexpr int BUF_ELEMS = 2 * K_ELEMS;
   constexpr int LOADS = K_ELEMS / 8 / kAttnThreads;
   constexpr int TILE_OPS = 2 * LOADS;
-  constexpr int STAGES = 4;
+  constexpr int STAGES = 5;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
-  __shared__ int rerun_flag;
+  // Between passes no tile is in flight, so the re-run vote borrows LDS.
+  int* const rerun_flag = reinterpret_cast<int*>(lds);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -424,8 +428,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kst, md), pb, oacc[md], 0, 0, 0);
     }
   };
-  // Barrier k publishes tile k and frees the stage of tile k-2, which tile
-  // k+2 refills.  Every wave meets it at the top of tile k.
+  // Barrier k publishes tile k and frees the stage of tile k-3, which tile
+  // k+2 refills (5 stages).  Waves 0-3 meet it at the top of tile k, waves
+  // 4-7 after their scores of tile k-1, so the two waves of a SIMD are half a
+  // tile apart.
   auto barrier_k = [&](int k) __attribute__((always_inline)) {
     publish_seq(k, min(n_tiles - 1 - k, 1));
     if (k + 2 < n_tiles) issue_seq(k + 2);
@@ -434,22 +440,24 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // block as this tile's probabilities (VALU), so one wave keeps both the
   // matrix and the vector units busy; the probabilities alternate between
   // two buffers.  Tile 0 has no predecessor.
+  const bool group_b = wave >= 4;
   auto first_tile = [&](bool masked) __attribute__((always_inline)) {
     barrier_k(0);
     scores(0, masked);
+    if (group_b && n_tiles > 1) barrier_k(1);
     probs(0, masked, -m_run);
     settle(0);
   };
   auto next_tile = [&](int i, int b, bool masked) __attribute__((always_inline)) {
-    barrier_k(i);
+    if (!group_b) barrier_k(i);
     scores(i, masked);
+    if (group_b && i + 1 < n_tiles) barrier_k(i + 1);
     pv(i - 1, b ^ 1);
     probs(b, masked, -m_run);
     settle(b);
   };
 
   for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
-    if (tid == 0) rerun_flag = 0;
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
     if (n_fast > 0) {
@@ -468,10 +476,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
     }
     pv(n_tiles - 1, 0);
-    if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(&rerun_flag, 1);
+    lds_barrier();  // every wave is done with the tiles
+    if (tid == 0) *rerun_flag = 0;
     lds_barrier();
-    const bool again = rerun_flag != 0;
+    if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(rerun_flag, 1);
     lds_barrier();
+    const bool again = *rerun_flag != 0;
+    lds_barrier();  // before the next pass's loads overwrite the flag
     if (!again) break;
     m_run = fmaxf(m_run, m_cand);
     m_cand = -INFINITY;
