@@ -13,7 +13,8 @@ Prints ONE JSON line:
              average launch duration (HIP events on the launch stream), against
              the bf16 dense MFMA peak
   cpu_baseline  the fp64 oracle on this host's cores over a bounded sample
-             of the same workload (every chunk x every head x 16 rows)
+             of the same workload (every chunk x every head x 64 rows, about ten
+             seconds on 16 cores)
 
 Usage: python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
@@ -42,7 +43,7 @@ def parse():
                     help="hold the KV of the first fraction of the sequence (whole blocks) in a second store, "
                          "as a debtor stage's remote portion, and read it with the two-store call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=16, help="oracle rows per (chunk, head)")
+    ap.add_argument("--cpu-rows", type=int, default=64, help="oracle rows per (chunk, head)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel for scaling a profiler's FETCH_SIZE / WRITE_SIZE counters)")
