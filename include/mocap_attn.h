@@ -272,6 +272,56 @@ mocap_status mocap_lbcp_plan(int64_t seq_len, int32_t num_chunks, int32_t num_st
                              double cost_pair, double cost_token, double cost_chunk,
                              int32_t* lengths_out, double* t_max_out, double* t_sum_out);
 
+/*
+ * mocap_lbcp_plan_table -- mocap_lbcp_plan with EvaluateChunk read from a
+ * table instead of the three-coefficient model (host only).
+ *
+ *   chunk_cost  host double [U][U] with U = seq_len / align:
+ *               chunk_cost[(k - 1) * U + s] is the latency of a chunk of
+ *               k * align tokens starting at token s * align, for k >= 1 and
+ *               s + k <= U (other entries are not read).  Typically measured
+ *               latencies interpolated over a grid.
+ * Other arguments and outputs as in mocap_lbcp_plan.
+ * Errors: as mocap_lbcp_plan, plus INVALID_ARG for a null table or a read
+ * entry that is negative or not finite.
+ */
+mocap_status mocap_lbcp_plan_table(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                                   const double* chunk_cost, int32_t* lengths_out, double* t_max_out,
+                                   double* t_sum_out);
+
+/*
+ * mocap_lbcp_refine -- second stage of latency-balanced chunk partitioning
+ * (Section 4.2, Alg. 1, the simulated-annealing refinement), host only.
+ *
+ * Starting from lengths_inout (typically the dynamic program's plan), the
+ * temperature runs from temp0, multiplied by alpha after every `rounds`
+ * perturbations, until it is no longer above temp_min.  A perturbation moves
+ * one of the num_chunks - 1 inner chunk boundaries by one align unit
+ * (seq_len and num_chunks preserved; a move that would empty a chunk is
+ * skipped).  A candidate is accepted if its latency T' is lower, or with
+ * probability exp(-(T' - T) / Temp); the best partition seen is returned.
+ * Random draws come from SplitMix64 seeded with `seed`: for each
+ * perturbation, one draw picks the boundary (draw mod (num_chunks - 1)), one
+ * the direction (lowest bit), and, for a valid move, one uniform in [0, 1)
+ * (the top 53 bits) the acceptance.
+ *
+ * The latency of a partition is its single-request prefill latency under
+ * the same table: sum of chunk costs + (num_stages - 1) * largest chunk cost.
+ * The paper's EvaluatePrefill / EvaluateE2E also model the feasible batch
+ * size and end-to-end queueing, which are outside this library.
+ *
+ *   chunk_cost     as in mocap_lbcp_plan_table
+ *   temp0 > 0, temp_min > 0, 0 < alpha < 1, rounds >= 1
+ *   lengths_inout  host int32 [num_chunks]: in, a partition of seq_len into
+ *                  positive multiples of align; out, the best one found
+ *   latency_out    (may be NULL) its latency
+ * Errors: INVALID_ARG for malformed sizes, table, schedule or input
+ * partition (nothing is written); UNSUPPORTED as in mocap_lbcp_plan.
+ */
+mocap_status mocap_lbcp_refine(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                               const double* chunk_cost, double temp0, double temp_min, double alpha,
+                               int32_t rounds, uint64_t seed, int32_t* lengths_inout, double* latency_out);
+
 /* A static, human-readable name for a status code. */
 const char* mocap_status_string(mocap_status status);
 

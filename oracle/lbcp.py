@@ -79,3 +79,73 @@ def brute_force(S, M, align, objective, evaluate):
         if best is None or val < best[0]:
             best = (val, lengths)
     return best
+
+
+# --- second stage: simulated annealing (Section 4.2, Alg. 1) --------------
+
+class SplitMix64:
+    """SplitMix64 (Steele, Lea and Flood, 2014), written from its definition:
+    the state advances by 0x9E3779B97F4A7C15 and each output is that state
+    through two xor-shift-multiply rounds and a final xor-shift."""
+    MASK = (1 << 64) - 1
+
+    def __init__(self, seed):
+        self.x = seed & self.MASK
+
+    def next(self):
+        self.x = (self.x + 0x9E3779B97F4A7C15) & self.MASK
+        z = self.x
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & self.MASK
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & self.MASK
+        return z ^ (z >> 31)
+
+    def uniform(self):
+        return (self.next() >> 11) * (1.0 / 9007199254740992.0)
+
+
+def prefill_latency(lengths_units, N, evaluate_units):
+    """Single-request pipeline latency of a partition: sum of chunk costs plus
+    (N - 1) times the largest (EvaluatePrefill without the batch model)."""
+    t_sum, t_max, s = 0.0, 0.0, 0
+    for k in lengths_units:
+        t = evaluate_units(k, s)
+        t_sum += t
+        t_max = max(t_max, t)
+        s += k
+    return t_sum + (N - 1) * t_max
+
+
+def lbcp_refine(S, M, N, align, lengths, temp0, temp_min, alpha, rounds, seed, evaluate):
+    """Alg. 1's second stage from an initial partition: while Temp > Temp_min,
+    R times: ss' = Perturb(ss) (one inner boundary moved by one align unit,
+    S and M preserved, moves that empty a chunk skipped); T' its latency;
+    accept if T' < T or Rand(0, 1) < exp(-(T' - T) / Temp); keep the best;
+    then Temp = alpha Temp.  evaluate(c, p) is in tokens.  Returns
+    (lengths, latency)."""
+    U = S // align
+    ev = lambda k, s: evaluate(k * align, s * align)
+    ss = [c // align for c in lengths]
+    assert sum(ss) == U and all(k >= 1 for k in ss)
+    rng = SplitMix64(seed)
+    T = prefill_latency(ss, N, ev)
+    best, T_best = list(ss), T
+    temp = temp0
+    while temp > temp_min:
+        for _ in range(rounds):
+            if M < 2:
+                break
+            j = 1 + rng.next() % (M - 1)            # boundary between chunks j-1 and j
+            step = 1 if rng.next() & 1 else -1       # +1 moves it right
+            cand = list(ss)
+            cand[j - 1] += step
+            cand[j] -= step
+            if cand[j - 1] < 1 or cand[j] < 1:
+                continue
+            T_new = prefill_latency(cand, N, ev)
+            u = rng.uniform()
+            if T_new < T or u < math.exp(-(T_new - T) / temp):
+                ss, T = cand, T_new
+            if T < T_best:
+                best, T_best = list(ss), T
+        temp *= alpha
+    return [k * align for k in best], T_best

@@ -8,7 +8,7 @@ missing this module raises instead of falling back to anything else.
 """
 import ctypes
 import os
-from typing import List, Optional, Tuple
+from typing import List, Optional, Sequence, Tuple
 
 import torch
 
@@ -30,6 +30,8 @@ EXPORTED = (
     "mocap_chunk_attn_two_store_workspace_size",
     "mocap_chunk_plan",
     "mocap_lbcp_plan",
+    "mocap_lbcp_plan_table",
+    "mocap_lbcp_refine",
     "mocap_status_string",
 )
 
@@ -97,6 +99,15 @@ def load_library():
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
         ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_int32),
         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    lib.mocap_lbcp_plan_table.restype = st
+    lib.mocap_lbcp_plan_table.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    lib.mocap_lbcp_refine.restype = st
+    lib.mocap_lbcp_refine.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32, ctypes.c_uint64,
+        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)]
     lib.mocap_chunk_plan.restype = st
     lib.mocap_chunk_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -263,3 +274,38 @@ def mocap_lbcp_plan(seq_len: int, num_chunks: int, num_stages: int, align: int, 
                                           float(cost_pair), float(cost_token), float(cost_chunk), out,
                                           ctypes.byref(t_max), ctypes.byref(t_sum)), "mocap_lbcp_plan")
     return list(out), t_max.value, t_sum.value
+
+
+def _cost_table(chunk_cost, units: int):
+    """A float64 [U][U] table as a ctypes pointer (the array must stay alive)."""
+    import numpy as np
+    arr = np.ascontiguousarray(chunk_cost, dtype=np.float64)
+    if arr.shape != (units, units):
+        raise ValueError(f"chunk_cost must be [{units}][{units}]")
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def mocap_lbcp_plan_table(seq_len: int, num_chunks: int, num_stages: int, align: int, chunk_cost):
+    """Returns (lengths, t_max, t_sum); chunk_cost[k - 1][s] in align units."""
+    arr, ptr = _cost_table(chunk_cost, seq_len // align)
+    out = (ctypes.c_int32 * num_chunks)()
+    t_max = ctypes.c_double(0.0)
+    t_sum = ctypes.c_double(0.0)
+    _check(load_library().mocap_lbcp_plan_table(int(seq_len), int(num_chunks), int(num_stages), int(align), ptr,
+                                                out, ctypes.byref(t_max), ctypes.byref(t_sum)),
+           "mocap_lbcp_plan_table")
+    return list(out), t_max.value, t_sum.value
+
+
+def mocap_lbcp_refine(seq_len: int, num_chunks: int, num_stages: int, align: int, chunk_cost,
+                      lengths: Sequence[int], temp0: float, temp_min: float, alpha: float, rounds: int,
+                      seed: int):
+    """Returns (lengths, latency) of the best partition the annealing found."""
+    arr, ptr = _cost_table(chunk_cost, seq_len // align)
+    io = (ctypes.c_int32 * num_chunks)(*[int(x) for x in lengths])
+    lat = ctypes.c_double(0.0)
+    _check(load_library().mocap_lbcp_refine(int(seq_len), int(num_chunks), int(num_stages), int(align), ptr,
+                                            float(temp0), float(temp_min), float(alpha), int(rounds),
+                                            int(seed) & 0xFFFFFFFFFFFFFFFF, io, ctypes.byref(lat)),
+           "mocap_lbcp_refine")
+    return list(io), lat.value

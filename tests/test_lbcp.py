@@ -176,3 +176,99 @@ def test_probe_plans_are_valid(mocap_lib):
     for lengths in plans:
         assert len(lengths) == 16 and sum(lengths) == 131072
         assert all(c > 0 and c % 128 == 0 for c in lengths)
+
+
+# --- stage 2: simulated annealing ----------------------------------------
+
+def _table(units, seed):
+    """A seeded non-linear, position-dependent cost table [k-1][s] (align units)."""
+    rng = random.Random(seed)
+    jitter = [[rng.uniform(0.0, 3.0) for _ in range(units)] for _ in range(units)]
+    t = [[0.0] * units for _ in range(units)]
+    for k in range(1, units + 1):
+        for s in range(units - k + 1):
+            t[k - 1][s] = k * k * 0.7 + k * s * 1.3 + 5.0 + jitter[k - 1][s]
+    return t
+
+
+def test_splitmix64_reference_outputs():
+    # First outputs of SplitMix64 from seed 0, as published with the
+    # generator's reference implementation.
+    g = lbcp.SplitMix64(0)
+    assert [g.next() for _ in range(3)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_refine_reaches_brute_force_optimum(seed):
+    U, M, N = 14, 4, 6
+    t = _table(U, seed)
+    ev = lambda c, p: t[c - 1][p]
+    start = [U - 3, 1, 1, 1]
+    lengths, lat = lbcp.lbcp_refine(U, M, N, 1, start, 200.0, 0.05, 0.97, 40, seed, ev)
+    best, _ = lbcp.brute_force(U, M, 1, lambda costs: sum(costs) + (N - 1) * max(costs), ev)
+    assert lat == pytest.approx(best, rel=1e-12)
+    assert lbcp.prefill_latency(lengths, N, lambda k, s: t[k - 1][s]) == lat
+
+
+def test_refine_at_zero_temperature_is_a_local_optimum():
+    # With a vanishing temperature only improvements are accepted: no single
+    # one-unit boundary move improves the result.
+    U, M, N = 20, 5, 8
+    t = _table(U, 9)
+    ev = lambda c, p: t[c - 1][p]
+    lengths, lat = lbcp.lbcp_refine(U, M, N, 1, [4] * 5, 1e-300, 1e-301, 0.5, 4000, 17, ev)
+    evu = lambda k, s: t[k - 1][s]
+    for j in range(1, M):
+        for step in (1, -1):
+            cand = list(lengths)
+            cand[j - 1] += step
+            cand[j] -= step
+            if min(cand) >= 1:
+                assert lbcp.prefill_latency(cand, N, evu) >= lat
+
+
+def test_refine_never_worse_than_its_start():
+    U, M, N = 30, 6, 4
+    t = _table(U, 4)
+    ev = lambda c, p: t[c - 1][p]
+    start = [5] * 6
+    lengths, lat = lbcp.lbcp_refine(U, M, N, 1, start, 50.0, 1.0, 0.9, 10, 5, ev)
+    assert sum(lengths) == U and min(lengths) >= 1
+    assert lat <= lbcp.prefill_latency(start, N, lambda k, s: t[k - 1][s])
+
+
+def test_library_table_dp_and_refine_match_oracle(mocap_lib):
+    import numpy as np
+    from paper_2606_22968_amd import binding
+    for U, M, N, align, seed in [(24, 5, 4, 64, 1), (40, 8, 16, 128, 2), (17, 1, 3, 32, 3), (33, 11, 2, 16, 4)]:
+        t = np.array(_table(U, seed))
+        ev = lambda c, p: float(t[c // align - 1][p // align])
+        got = binding.mocap_lbcp_plan_table(U * align, M, N, align, t)
+        want = lbcp.lbcp_dp(U * align, M, N, align, evaluate=ev)
+        assert got[0] == want[0] and got[1] == want[1] and got[2] == want[2]
+        for sa_seed in (7, 8):
+            got_r = binding.mocap_lbcp_refine(U * align, M, N, align, t, got[0], 30.0, 0.5, 0.9, 12, sa_seed)
+            want_r = lbcp.lbcp_refine(U * align, M, N, align, got[0], 30.0, 0.5, 0.9, 12, sa_seed, ev)
+            assert got_r[0] == want_r[0] and got_r[1] == want_r[1], (U, M, seed, sa_seed)
+
+
+def test_refine_and_table_validation(mocap_lib):
+    import numpy as np
+    from paper_2606_22968_amd import binding
+    t = np.ones((8, 8))
+    with pytest.raises(binding.MocapError):
+        binding.mocap_lbcp_refine(512, 2, 2, 64, t, [256, 255], 1.0, 0.1, 0.5, 1, 0)   # not aligned
+    with pytest.raises(binding.MocapError):
+        binding.mocap_lbcp_refine(512, 2, 2, 64, t, [256, 128], 1.0, 0.1, 0.5, 1, 0)   # wrong total
+    with pytest.raises(binding.MocapError):
+        binding.mocap_lbcp_refine(512, 2, 2, 64, t, [256, 256], 1.0, 0.1, 1.0, 1, 0)   # alpha >= 1
+    with pytest.raises(binding.MocapError):
+        binding.mocap_lbcp_refine(512, 2, 2, 64, t, [256, 256], 0.0, 0.1, 0.5, 1, 0)   # temp0 <= 0
+    bad = t.copy()
+    bad[0][3] = np.nan
+    with pytest.raises(binding.MocapError):
+        binding.mocap_lbcp_plan_table(512, 2, 2, 64, bad)
+    bad[0][3] = 1.0
+    bad[7][1] = np.nan   # k = 8, s = 1: never read (k + s > U), so accepted
+    lengths, _, _ = binding.mocap_lbcp_plan_table(512, 2, 2, 64, bad)
+    assert sum(lengths) == 512 and min(lengths) >= 64
