@@ -151,6 +151,121 @@ def measure_layer(shape, plans: Sequence[Sequence[int]], reps: int = 3, seed: in
     return out
 
 
+def measure_grid(shape, seq_len: int, c_grid: Sequence[int], p_fracs: Sequence[float], align: int,
+                 reps: int = 3, seed: int = 0, block_size: int = 256, attn=None):
+    """Latency (microseconds) of single chunks at chosen (length, prefix)
+    points, every chunk run against one store holding the whole sequence:
+    for each c in c_grid, prefixes round(f (S - c)) to multiples of align for
+    f in p_fracs.  shape: a layer.LayerShape (whole decoder layer per chunk)
+    or None with attn = (h_q, h_kv, head_dim, scale) (append + attention).
+    Returns {(c, p): us}."""
+    import torch
+
+    from . import synth
+    from .layer import ChunkedLayer
+    from .prefill import ChunkedPrefill
+
+    stream = torch.cuda.current_stream()
+    if shape is not None:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(seed)
+        x = torch.randn((seq_len, shape.hidden), generator=g, dtype=torch.float32).to(torch.bfloat16).cuda()
+        runner = ChunkedLayer(shape, [seq_len], seed=seed, block_size=block_size)
+        scale = shape.head_dim ** -0.5
+        runner.run(x, scale, stream=stream)  # fills the whole store once
+
+        def one(c, p):
+            xc = x[p:p + c]
+            q, k, v = runner.project_qkv(xc)
+            binding.mocap_kv_append(runner.attn.store, runner.attn.table, p, k, v, stream)
+            o = torch.empty((c, shape.h_q, shape.head_dim), dtype=torch.bfloat16, device="cuda")
+            lse = torch.empty((shape.h_q, c), dtype=torch.float32, device="cuda")
+            binding.mocap_chunk_attn(runner.attn.store, runner.attn.table, q, p, scale, o, lse,
+                                     ws_for(p, c, shape.h_q, shape.h_kv, shape.head_dim), 0, stream)
+            y = xc + o.reshape(c, -1) @ runner.w_o
+            gu = y @ runner.w_gu
+            h = torch.nn.functional.silu(gu[:, :shape.ffn]) * gu[:, shape.ffn:]
+            return y + h @ runner.w_d
+    else:
+        h_q, h_kv, d, scale = attn
+        q, k, v = (t.cuda() for t in synth.make_qkv(seed, seq_len, h_q, h_kv, d))
+        runner = ChunkedPrefill(h_q, h_kv, d, [seq_len], block_size=block_size)
+        runner.run(q, k, v, scale, stream=stream)
+
+        def one(c, p):
+            binding.mocap_kv_append(runner.store, runner.table, p, k[p:p + c], v[p:p + c], stream)
+            o = torch.empty((c, h_q, d), dtype=torch.bfloat16, device="cuda")
+            lse = torch.empty((h_q, c), dtype=torch.float32, device="cuda")
+            binding.mocap_chunk_attn(runner.store, runner.table, q[p:p + c], p, scale, o, lse,
+                                     ws_for(p, c, h_q, h_kv, d), 0, stream)
+            return o
+
+    workspaces = {}
+
+    def ws_for(p, c, h_q, h_kv, d):
+        _, nbytes = binding.mocap_chunk_attn_workspace_size(p, c, h_q, h_kv, d, 0)
+        if nbytes not in workspaces:
+            workspaces[nbytes] = torch.empty(max(nbytes, 16), dtype=torch.uint8, device="cuda")
+        return workspaces[nbytes]
+
+    out = {}
+    for c in c_grid:
+        for f in p_fracs:
+            p = int(round(f * (seq_len - c) / align)) * align
+            if (c, p) in out:
+                continue
+            one(c, p)  # warm-up
+            times = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                one(c, p)
+                e1.record(stream)
+                e1.synchronize()
+                times.append(e0.elapsed_time(e1) * 1e3)
+            out[(c, p)] = statistics.median(times)
+    return out
+
+
+def cost_table(grid, model: LatencyModel, seq_len: int, align: int):
+    """Chunk-cost table [k - 1][s] (align units) for mocap_lbcp_plan_table:
+    the fitted model times a measured correction, interpolated linearly in
+    chunk length between grid lengths and, for each grid length, linearly in
+    the prefix fraction p / (S - c)."""
+    import numpy as np
+
+    U = seq_len // align
+    lengths = sorted({c for c, _ in grid})
+    corr = {}
+    for c in lengths:
+        pts = sorted((p / max(seq_len - c, 1), t / model(c, p)) for (cc, p), t in grid.items() if cc == c)
+        corr[c] = ([x for x, _ in pts], [y for _, y in pts])
+
+    def factor(c, p):
+        frac = p / max(seq_len - c, 1)
+        if c <= lengths[0]:
+            lo = hi = lengths[0]
+        elif c >= lengths[-1]:
+            lo = hi = lengths[-1]
+        else:
+            hi = next(x for x in lengths if x >= c)
+            lo = max(x for x in lengths if x <= c)
+        f_lo = float(np.interp(frac, *corr[lo]))
+        f_hi = float(np.interp(frac, *corr[hi]))
+        if hi == lo:
+            return f_lo
+        w = (c - lo) / (hi - lo)
+        return f_lo * (1 - w) + f_hi * w
+
+    table = np.zeros((U, U), dtype=np.float64)
+    for k in range(1, U + 1):
+        c = k * align
+        for s in range(U - k + 1):
+            p = s * align
+            table[k - 1, s] = model(c, p) * factor(c, p)
+    return table
+
+
 def _objective(latencies: Sequence[float], num_stages: int) -> float:
     return sum(latencies) + (num_stages - 1) * max(latencies)
 
@@ -170,6 +285,10 @@ def main(argv=None):
     ap.add_argument("--align", type=int, default=0, help="0 = the workload's alignment")
     ap.add_argument("--reps", type=int, default=3)
     ap.add_argument("--random-plans", type=int, default=4)
+    ap.add_argument("--stage2", action="store_true",
+                    help="also build a measured chunk-cost table over a (length, prefix) grid, run the "
+                         "table-driven dynamic program and the simulated-annealing refinement, and "
+                         "measure their plans")
     args = ap.parse_args(argv)
 
     w = synth.WORKLOADS[args.workload]
@@ -191,8 +310,26 @@ def main(argv=None):
     model = fit([(c, p, t) for _, c, p, t, _, _ in samples])
     dp_lengths, t_max, t_sum = plan(seq_len, m, args.stages, align, model)
     closed = probes[1]
-    print("[lbcp] measuring the closed-form and dynamic-programming plans", file=sys.stderr, flush=True)
-    final = timed([closed, dp_lengths])
+    plans = [closed, dp_lengths]
+    stage2 = None
+    if args.stage2:
+        c_grid = [c for c in (128, 256, 384, 512, 768, 1024, 1536, 2048, 3072, 4096, 6144, 8192, 12288, 16384,
+                              24576, 32768, 49152, 65536) if c % align == 0 and c <= seq_len - (m - 1) * align]
+        print(f"[lbcp] measuring a {len(c_grid)} x 6 (length, prefix) grid", file=sys.stderr, flush=True)
+        attn = None if shape else (w.h_q, w.h_kv, w.head_dim, w.scale)
+        grid = measure_grid(shape, seq_len, c_grid, (0.0, 0.125, 0.25, 0.5, 0.75, 1.0), align, args.reps,
+                            w.seed, w.block_size, attn=attn)
+        table = cost_table(grid, model, seq_len, align)
+        table_lengths, tt_max, tt_sum = binding.mocap_lbcp_plan_table(seq_len, m, args.stages, align, table)
+        t0 = tt_sum + (args.stages - 1) * tt_max
+        sa_lengths, sa_lat = binding.mocap_lbcp_refine(seq_len, m, args.stages, align, table, table_lengths,
+                                                       temp0=0.01 * t0, temp_min=1e-5 * t0, alpha=0.95,
+                                                       rounds=50, seed=w.seed)
+        stage2 = {"grid_points": len(grid), "table_dp_model_us": round(t0, 1),
+                  "refined_model_us": round(sa_lat, 1)}
+        plans += [table_lengths, sa_lengths]
+    print("[lbcp] measuring the candidate plans", file=sys.stderr, flush=True)
+    final = timed(plans)
 
     def summary(i, lengths):
         rows = [x for x in final if x[0] == i]
@@ -210,6 +347,8 @@ def main(argv=None):
         "closed_form": summary(0, closed),
         "dp": dict(summary(1, dp_lengths), model_t_max_us=round(t_max, 1), model_t_sum_us=round(t_sum, 1)),
     }
+    if stage2 is not None:
+        report["stage2"] = dict(stage2, table_dp=summary(2, plans[2]), refined=summary(3, plans[3]))
     print(json.dumps(report), flush=True)
     return report
 

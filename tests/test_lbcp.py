@@ -272,3 +272,23 @@ def test_refine_and_table_validation(mocap_lib):
     bad[7][1] = np.nan   # k = 8, s = 1: never read (k + s > U), so accepted
     lengths, _, _ = binding.mocap_lbcp_plan_table(512, 2, 2, 64, bad)
     assert sum(lengths) == 512 and min(lengths) >= 64
+
+
+def test_cost_table_interpolates_the_measured_correction():
+    from paper_2606_22968_amd import lbcp as plbcp
+    model = plbcp.LatencyModel(2e-6, 1e-2, 30.0, 0.0)
+    S, align = 4096, 128
+    c_grid = [128, 512, 2048, 4096 - 128]
+    grid = {}
+    for c in c_grid:
+        for f in (0.0, 0.5, 1.0):
+            p = int(round(f * (S - c) / align)) * align
+            grid[(c, p)] = model(c, p) * (1.5 if c >= 2048 else 1.0)
+    t = plbcp.cost_table(grid, model, S, align)
+    U = S // align
+    assert t.shape == (U, U)
+    assert t[0, 5] == pytest.approx(model(128, 5 * 128))               # factor 1 at a grid length
+    assert t[2048 // 128 - 1, 3] == pytest.approx(1.5 * model(2048, 3 * 128))
+    k = 1280 // 128  # halfway between 512 and 2048: factor 1.25
+    assert t[k - 1, 7] == pytest.approx(1.25 * model(1280, 7 * 128))
+    assert t[U - 1, 0] > 0 and t[0, U - 1] > 0
