@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmocap_attn.so")
-SOURCES = ["api.cpp", "chunk_attn.hip", "kv_append.hip", "lse_merge.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "chunk_attn.hip", "kv_append.hip", "lse_merge.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -1,0 +1,234 @@
+// Host-side chunk planners of libmocap_attn (no device work): the closed-form
+// balanced chunk plan and the latency-balanced chunk partitioning of the
+// paper's Section 4.2 (Alg. 1: the dynamic program and the simulated-annealing
+// refinement).
+#include "mocap_attn.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <vector>
+
+namespace {
+
+// Sizes shared by the LBCP planners: S a positive multiple of align, M
+// chunks of at least one align unit, N >= 1 stages, and a table small
+// enough to scan (M (S / align)^2 <= 2^31).
+mocap_status check_lbcp_sizes(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align) {
+  if (seq_len <= 0 || num_chunks <= 0 || num_stages <= 0 || align <= 0) return MOCAP_ERR_INVALID_ARG;
+  if (seq_len % align != 0 || (int64_t)num_chunks * align > seq_len) return MOCAP_ERR_INVALID_ARG;
+  const int64_t U = seq_len / align;
+  if (U > 0x7fffffff / align) return MOCAP_ERR_INVALID_ARG;
+  if ((double)num_chunks * (double)U * (double)U > 2147483648.0) return MOCAP_ERR_UNSUPPORTED;
+  return MOCAP_OK;
+}
+
+// A chunk-cost table [k - 1][s] (k units long, starting at unit s) must be
+// finite and non-negative wherever k + s <= U.
+bool valid_cost_table(const double* cost, int64_t U) {
+  for (int64_t k = 1; k <= U; ++k)
+    for (int64_t s = 0; s + k <= U; ++s) {
+      const double t = cost[(size_t)(k - 1) * U + (size_t)s];
+      if (!(t >= 0.0) || !std::isfinite(t)) return false;
+    }
+  return true;
+}
+
+// Alg. 1, lines 1-7 (Section 4.2): for chunk index m from M down to 1, start
+// u from U - 1 down to 0 and length k upwards, combine EvaluateChunk(k, u)
+// with the suffix state (m + 1, u + k) and keep the k minimising
+// t'_sum + (N - 1) t'_max.  The suffix boundary is t = 0 at (M + 1, U) and
+// infeasible elsewhere.
+template <typename Eval>
+mocap_status lbcp_dp(int64_t U, int M, int num_stages, int32_t align, Eval evaluate, int32_t* lengths_out,
+                     double* t_max_out, double* t_sum_out) {
+#pragma clang fp contract(off)
+  const double stages_m1 = (double)(num_stages - 1);
+  const double inf = INFINITY;
+  std::vector<double> tmax((size_t)(M + 2) * (U + 1), inf), tsum((size_t)(M + 2) * (U + 1), inf);
+  std::vector<int32_t> ss((size_t)(M + 2) * (U + 1), 0);
+  auto at = [&](int m, int64_t u) { return (size_t)m * (U + 1) + (size_t)u; };
+  tmax[at(M + 1, U)] = 0.0;
+  tsum[at(M + 1, U)] = 0.0;
+  for (int m = M; m >= 1; --m) {
+    for (int64_t s = U - 1; s >= 0; --s) {
+      double best_obj = inf;
+      for (int64_t k = 1; k <= U - s - (M - m); ++k) {
+        const size_t nxt = at(m + 1, s + k);
+        if (tsum[nxt] == inf) continue;  // infeasible suffix
+        const double t = evaluate(k, s);
+        const double t_max = std::max(tmax[nxt], t);
+        const double t_sum = tsum[nxt] + t;
+        const double obj = t_sum + stages_m1 * t_max;
+        if (obj < best_obj) {
+          best_obj = obj;
+          tmax[at(m, s)] = t_max;
+          tsum[at(m, s)] = t_sum;
+          ss[at(m, s)] = (int32_t)k;
+        }
+      }
+    }
+  }
+  if (tsum[at(1, 0)] == inf) return MOCAP_ERR_INVALID_ARG;
+  int64_t u = 0;
+  for (int m = 1; m <= M; ++m) {
+    const int32_t k = ss[at(m, u)];
+    lengths_out[m - 1] = k * align;
+    u += k;
+  }
+  if (t_max_out) *t_max_out = tmax[at(1, 0)];
+  if (t_sum_out) *t_sum_out = tsum[at(1, 0)];
+  return MOCAP_OK;
+}
+
+// SplitMix64 (Steele, Lea and Flood, 2014): a counter-based generator,
+// x += 0x9E3779B97F4A7C15 then two xor-shift-multiply rounds.
+struct SplitMix64 {
+  uint64_t x;
+  uint64_t next() {
+    uint64_t z = (x += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  }
+  double uniform() { return (double)(next() >> 11) * (1.0 / 9007199254740992.0); }  // [0, 1), 53 bits
+};
+
+}  // namespace
+
+extern "C" {
+
+mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align, int32_t balanced,
+                              int32_t* lengths_out) {
+  if (seq_len <= 0 || num_chunks <= 0 || lengths_out == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (seq_len > ((int64_t)1 << 40)) return MOCAP_ERR_INVALID_ARG;
+  typedef __int128 i128;
+  int64_t prev = 0;
+  for (int c = 1; c <= num_chunks; ++c) {
+    int64_t bound;
+    if (c == num_chunks) {
+      bound = seq_len;
+    } else if (!balanced) {
+      bound = (int64_t)((i128)c * seq_len / num_chunks);
+    } else {
+      if (align <= 0 || seq_len % align != 0) return MOCAP_ERR_INVALID_ARG;
+      // Boundary in units of `align`: u = A sqrt(c / M) with A = seq_len / align.
+      // The nearest integer k satisfies M (2k - 1)^2 <= 4 A^2 c < M (2k + 1)^2.
+      const i128 A = seq_len / align;
+      const i128 rhs = 4 * A * A * (i128)c;
+      int64_t k = (int64_t)std::floor((double)A * std::sqrt((double)c / num_chunks) + 0.5);
+      auto lower_ok = [&](int64_t kk) { return kk <= 0 || (i128)num_chunks * (2 * (i128)kk - 1) * (2 * (i128)kk - 1) <= rhs; };
+      while (!lower_ok(k)) --k;
+      while (lower_ok(k + 1)) ++k;
+      const i128 edge = (i128)num_chunks * (2 * (i128)k - 1) * (2 * (i128)k - 1);
+      if (k > 0 && edge == rhs) return MOCAP_ERR_INVALID_ARG;  // exact tie
+      bound = k * (int64_t)align;
+    }
+    const int64_t len = bound - prev;
+    if (len <= 0 || len > 0x7fffffff) return MOCAP_ERR_INVALID_ARG;
+    lengths_out[c - 1] = (int32_t)len;
+    prev = bound;
+  }
+  return MOCAP_OK;
+}
+
+mocap_status mocap_lbcp_plan(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                             double cost_pair, double cost_token, double cost_chunk,
+                             int32_t* lengths_out, double* t_max_out, double* t_sum_out) {
+#pragma clang fp contract(off)
+  if (!(cost_pair >= 0.0) || !(cost_token >= 0.0) || !(cost_chunk >= 0.0) || !std::isfinite(cost_pair) ||
+      !std::isfinite(cost_token) || !std::isfinite(cost_chunk))
+    return MOCAP_ERR_INVALID_ARG;
+  const mocap_status st = check_lbcp_sizes(seq_len, num_chunks, num_stages, align);
+  if (st != MOCAP_OK || lengths_out == nullptr) return st != MOCAP_OK ? st : MOCAP_ERR_INVALID_ARG;
+  return lbcp_dp(seq_len / align, num_chunks, num_stages, align,
+                 [&](int64_t k, int64_t s) {
+                   const double c = (double)(k * align), p = (double)(s * align);
+                   return cost_pair * (c * p + c * (c + 1.0) / 2.0) + cost_token * c + cost_chunk;
+                 },
+                 lengths_out, t_max_out, t_sum_out);
+}
+
+mocap_status mocap_lbcp_plan_table(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                                   const double* chunk_cost, int32_t* lengths_out, double* t_max_out,
+                                   double* t_sum_out) {
+#pragma clang fp contract(off)
+  const mocap_status st = check_lbcp_sizes(seq_len, num_chunks, num_stages, align);
+  if (st != MOCAP_OK) return st;
+  if (chunk_cost == nullptr || lengths_out == nullptr) return MOCAP_ERR_INVALID_ARG;
+  const int64_t U = seq_len / align;
+  if (!valid_cost_table(chunk_cost, U)) return MOCAP_ERR_INVALID_ARG;
+  return lbcp_dp(U, num_chunks, num_stages, align,
+                 [&](int64_t k, int64_t s) { return chunk_cost[(size_t)(k - 1) * U + (size_t)s]; },
+                 lengths_out, t_max_out, t_sum_out);
+}
+
+mocap_status mocap_lbcp_refine(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                               const double* chunk_cost, double temp0, double temp_min, double alpha,
+                               int32_t rounds, uint64_t seed, int32_t* lengths_inout, double* latency_out) {
+#pragma clang fp contract(off)
+  mocap_status st = check_lbcp_sizes(seq_len, num_chunks, num_stages, align);
+  if (st != MOCAP_OK) return st;
+  if (chunk_cost == nullptr || lengths_inout == nullptr) return MOCAP_ERR_INVALID_ARG;
+  if (!(temp0 > 0.0) || !(temp_min > 0.0) || !std::isfinite(temp0) || !(alpha > 0.0) || !(alpha < 1.0) ||
+      rounds < 1)
+    return MOCAP_ERR_INVALID_ARG;
+  const int64_t U = seq_len / align;
+  if (!valid_cost_table(chunk_cost, U)) return MOCAP_ERR_INVALID_ARG;
+  const int M = num_chunks;
+  // Chunk lengths in units of align; must be a valid partition of seq_len.
+  std::vector<int64_t> ss(M);
+  int64_t total = 0;
+  for (int m = 0; m < M; ++m) {
+    if (lengths_inout[m] <= 0 || lengths_inout[m] % align != 0) return MOCAP_ERR_INVALID_ARG;
+    ss[m] = lengths_inout[m] / align;
+    total += ss[m];
+  }
+  if (total != U) return MOCAP_ERR_INVALID_ARG;
+  // Pipeline latency of a partition: sum of its chunk costs plus (N - 1)
+  // times the largest (Alg. 1's first-stage objective, here evaluated
+  // exactly on the whole partition).
+  const double stages_m1 = (double)(num_stages - 1);
+  auto latency = [&](const std::vector<int64_t>& x) {
+    double t_sum = 0.0, t_max = 0.0;
+    int64_t s = 0;
+    for (int m = 0; m < M; ++m) {
+      const double t = chunk_cost[(size_t)(x[m] - 1) * U + (size_t)s];
+      t_sum += t;
+      t_max = std::max(t_max, t);
+      s += x[m];
+    }
+    return t_sum + stages_m1 * t_max;
+  };
+  SplitMix64 rng{seed};
+  std::vector<int64_t> best = ss, cand = ss;
+  double t_cur = latency(ss), t_best = t_cur;
+  for (double temp = temp0; temp > temp_min; temp *= alpha) {
+    for (int r = 0; r < rounds; ++r) {
+      // Perturb: move one of the M - 1 inner boundaries by one unit, keeping
+      // both neighbouring chunks non-empty (S and M are preserved).
+      if (M < 2) break;
+      const int64_t j = 1 + (int64_t)(rng.next() % (uint64_t)(M - 1));  // boundary between chunks j-1 and j
+      const int64_t dir = (rng.next() & 1) ? 1 : -1;                     // +1 moves the boundary right
+      cand = ss;
+      cand[j - 1] += dir;
+      cand[j] -= dir;
+      if (cand[j - 1] < 1 || cand[j] < 1) continue;
+      const double t_new = latency(cand);
+      const double u = rng.uniform();
+      if (t_new < t_cur || u < std::exp(-(t_new - t_cur) / temp)) {
+        ss = cand;
+        t_cur = t_new;
+      }
+      if (t_cur < t_best) {
+        best = ss;
+        t_best = t_cur;
+      }
+    }
+  }
+  for (int m = 0; m < M; ++m) lengths_inout[m] = (int32_t)(best[m] * align);
+  if (latency_out) *latency_out = t_best;
+  return MOCAP_OK;
+}
+
+}  // extern "C"
