@@ -34,7 +34,7 @@ bool valid_cost_table(const double* cost, int64_t U) {
   return true;
 }
 
-// Alg. 1, lines 1-7 (Section 4.2): for chunk index m from M down to 1, start
+// Alg. 1, first stage (Section 4.2): for chunk index m from M down to 1, start
 // u from U - 1 down to 0 and length k upwards, combine EvaluateChunk(k, u)
 // with the suffix state (m + 1, u + k) and keep the k minimising
 // t'_sum + (N - 1) t'_max.  The suffix boundary is t = 0 at (M + 1, U) and
