@@ -32,7 +32,8 @@ def test_reduced_model_shapes_all_rows(gpu, oracle_lib, h_q, h_kv, d, lengths):
     check_chunks(oracle_lib, runner, q, k, v, scale, label=f"reduced {h_q}/{h_kv}/{d}")
 
 
-@pytest.mark.parametrize("h_q,h_kv,d", [(8, 8, 64), (8, 4, 128), (8, 2, 128), (16, 2, 64), (12, 4, 128)])
+@pytest.mark.parametrize("h_q,h_kv,d", [(8, 8, 64), (8, 4, 128), (8, 2, 128), (16, 2, 64), (12, 4, 128),
+                                        (32, 1, 128), (64, 1, 64), (6, 3, 128)])
 def test_ragged_chunks_all_rows(gpu, oracle_lib, h_q, h_kv, d):
     # Chunk and prefix lengths that are not multiples of the 64-key tile, a
     # store of 64-position blocks, and NaN in every unwritten pool slot.
