@@ -160,8 +160,9 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
  * mocap_chunk_attn_two_store -- mocap_chunk_attn for a chunk whose prefix KV
  * lives partly in a second store: the memory-balanced KV reallocation of
  * Section 4.1, where a debtor stage's KV accesses split into a remote portion
- * (held by its paired creditor stage) and a local portion, combined here by
- * the log-sum-exp merge of the split ranges.
+ * (held by its paired creditor stage) and a local portion.  The attention
+ * kernel picks the store for every 64-key tile it loads, so the result does
+ * not depend on where the range edges fall.
  *
  *   kv, block_table, n_table   the first ("local") store: it holds positions
  *               [0, remote_begin) and [remote_end, prefix_len + chunk_len),
@@ -179,19 +180,13 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
  *               remote_end <= prefix_len.  An empty range makes the call
  *               identical to mocap_chunk_attn (remote arguments unused, may
  *               be NULL).
- *   num_splits  total number of KV ranges, or 0 to let the library choose;
- *               raised to at least one prefix range per non-empty segment
- *               ([0, remote_begin), the remote range, [remote_end,
- *               prefix_len)) plus the chunk's own range, and clamped to what
- *               the prefix allows.  Prefix ranges are shared out among the
- *               segments in proportion to their lengths.
- *   other arguments as in mocap_chunk_attn; the workspace must hold
- *   mocap_chunk_attn_two_store_workspace_size bytes.
+ *   num_splits, workspace, other arguments   as in mocap_chunk_attn (the
+ *               split plan is the same as for a single store).
  *
  * Each store is read only at the positions it holds, so the other store's
- * slots at those positions may hold anything (NaN included).  Results equal
- * mocap_chunk_attn's within the tolerance of a split; they are bitwise equal
- * to a single-store call whose split plan has the same range edges.
+ * slots at those positions may hold anything (NaN included).  Results are
+ * bitwise equal to mocap_chunk_attn's on a single store holding the same
+ * keys and values, with the same num_splits.
  * Errors: as mocap_chunk_attn, plus INVALID_ARG for a malformed remote range,
  * a remote store that differs in h_kv, head_dim or block_size, or a remote
  * table that is too short or null.
@@ -206,8 +201,9 @@ mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t*
 
 /*
  * mocap_chunk_attn_two_store_workspace_size -- the range count and workspace
- * bytes of mocap_chunk_attn_two_store for the same shape, remote range and
- * num_splits (see above).  splits_out may be NULL.
+ * bytes of mocap_chunk_attn_two_store: the same as
+ * mocap_chunk_attn_workspace_size for the shape, after the remote range is
+ * checked.  splits_out may be NULL.
  * Errors: INVALID_ARG for a null bytes_out, malformed sizes or remote range;
  * UNSUPPORTED for head_dim not in {64, 128}; HIP if the device query fails
  * (num_splits = 0 only).

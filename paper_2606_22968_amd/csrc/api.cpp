@@ -58,11 +58,8 @@ struct Plan {
   int64_t prefix_tiles;
   int n_ranges;
   size_t ws_bytes;
-  // Prefix tiles [remote_begin, remote_end) come from a second store; the
-  // prefix ranges are parts_before over [0, remote_begin), parts_remote over
-  // the second store's tiles and the rest over [remote_end, prefix_tiles).
+  // Prefix tiles [remote_begin, remote_end) come from a second store.
   int64_t remote_begin = 0, remote_end = 0;
-  int parts_before = 0, parts_remote = 0;
 };
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -205,44 +202,6 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
   return MOCAP_OK;
 }
 
-// Plan of a chunk whose prefix keys [64 tb, 64 te) live in a second store
-// (tb < te): the plan of make_plan for the same shape, with at least one
-// prefix range per non-empty segment (before, second store, after).  The
-// prefix ranges are shared out one by one to the segment with the most tiles
-// per range, never more ranges than tiles in a segment.
-mocap_status make_two_store_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
-                                 int32_t head_dim, int32_t num_splits, int64_t tb, int64_t te, Plan* plan) {
-  mocap_status st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, plan);
-  if (st != MOCAP_OK) return st;
-  const int64_t tiles[3] = {tb, te - tb, plan->prefix_tiles - te};
-  int parts[3] = {0, 0, 0};
-  int64_t wanted = plan->n_ranges - 1, segments = 0;
-  for (int i = 0; i < 3; ++i) {
-    if (tiles[i] > 0) {
-      parts[i] = 1;
-      ++segments;
-    }
-  }
-  wanted = std::min<int64_t>(std::max<int64_t>(wanted, segments), plan->prefix_tiles);
-  for (int64_t given = segments; given < wanted; ++given) {
-    int best = -1;
-    for (int i = 0; i < 3; ++i) {
-      if (parts[i] == 0 || parts[i] >= tiles[i]) continue;
-      // tiles[i] / parts[i] > tiles[best] / parts[best], in integers
-      if (best < 0 || tiles[i] * parts[best] > tiles[best] * parts[i]) best = i;
-    }
-    if (best < 0) break;
-    ++parts[best];
-  }
-  plan->parts_before = parts[0];
-  plan->parts_remote = parts[1];
-  plan->remote_begin = tb;
-  plan->remote_end = te;
-  plan->n_ranges = parts[0] + parts[1] + parts[2] + 1;
-  plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
-  return MOCAP_OK;
-}
-
 mocap_status check_store(const mocap_kv_store* kv) {
   if (kv == nullptr) return MOCAP_ERR_INVALID_ARG;
   if (kv->num_blocks <= 0 || kv->block_size <= 0 || kv->h_kv <= 0 || kv->head_dim <= 0)
@@ -323,8 +282,6 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   p.n_ranges = plan.n_ranges;
   p.remote_begin = (int32_t)plan.remote_begin;
   p.remote_end = (int32_t)plan.remote_end;
-  p.parts_before = plan.parts_before;
-  p.parts_remote = plan.parts_remote;
   p.total_wgs = (int)total;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
   p.ws_o = nullptr;
@@ -446,11 +403,7 @@ mocap_status mocap_chunk_attn_two_store_workspace_size(int64_t prefix_len, int32
     return MOCAP_OK;
   }
   Plan plan;
-  const mocap_status st =
-      remote_begin == remote_end
-          ? make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan)
-          : make_two_store_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits,
-                                remote_begin / kTileKeys, remote_end / kTileKeys, &plan);
+  const mocap_status st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
   if (st != MOCAP_OK) return st;
   if (splits_out) *splits_out = plan.n_ranges;
   *bytes_out = plan.ws_bytes;
@@ -488,9 +441,10 @@ mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t*
       !aligned16(remote_kv->v_pool) || !aligned16(remote_table))
     return MOCAP_ERR_INVALID_ARG;
   Plan plan;
-  st = make_two_store_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, remote_begin / kTileKeys,
-                           remote_end / kTileKeys, &plan);
+  st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
   if (st != MOCAP_OK) return st;
+  plan.remote_begin = remote_begin / kTileKeys;
+  plan.remote_end = remote_end / kTileKeys;
   return enqueue_attention(kv, block_table, remote_kv, remote_table, plan, q, prefix_len, chunk_len, h_q, h_kv,
                            head_dim, scale, o, lse, workspace, workspace_bytes, stream);
 }

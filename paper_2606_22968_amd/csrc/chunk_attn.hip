@@ -37,10 +37,9 @@
 //     (unwritten store memory) are zero-filled in LDS so a masked probability
 //     of 0 never meets a NaN.
 //   * Optional split of the prefix into ranges: each range writes normalised
-//     fp32 partials and their log-sum-exp; lse_merge.hip combines them.  A
-//     run of prefix tiles may come from a second store (a debtor stage's
-//     remote KV portion, Section 4.1); its ranges read that store's pools
-//     and block table instead.
+//     fp32 partials and their log-sum-exp; lse_merge.hip combines them.
+//   * A run of prefix tiles may come from a second store (a debtor stage's
+//     remote KV portion, Section 4.1): the store is chosen per tile.
 #include "internal.h"
 
 #include <math.h>
@@ -189,31 +188,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const int wg_row_end = min(L, (item.row_group + 1) * blocks_per_wg * kAttnWaveRows);
 
   int lo, hi;
-  bool second_store = false;
   if (p.n_ranges == 1) {
     lo = 0;
     hi = P + L;
   } else if (item.range < p.n_ranges - 1) {
-    // Prefix range: segment [seg_lo, seg_hi) of tiles cut into `parts`.
-    int r = item.range, seg_lo, seg_hi, parts;
-    if (r < p.parts_before) {
-      seg_lo = 0, seg_hi = p.remote_begin, parts = p.parts_before;
-    } else if ((r -= p.parts_before) < p.parts_remote) {
-      seg_lo = p.remote_begin, seg_hi = p.remote_end, parts = p.parts_remote;
-      second_store = true;
-    } else {
-      r -= p.parts_remote;
-      seg_lo = p.remote_end, seg_hi = p.prefix_tiles, parts = p.n_ranges - 1 - p.parts_before - p.parts_remote;
-    }
-    const int64_t span = seg_hi - seg_lo;
-    lo = (int)(seg_lo + span * r / parts) * kTileKeys;
-    hi = min((int)(seg_lo + span * (r + 1) / parts) * kTileKeys, P);
+    const int parts = p.n_ranges - 1;
+    lo = (int)((int64_t)p.prefix_tiles * item.range / parts) * kTileKeys;
+    hi = min((int)((int64_t)p.prefix_tiles * (item.range + 1) / parts) * kTileKeys, P);
   } else {
     lo = P;
     hi = P + L;
   }
-  const uint16_t* const k_pool = second_store ? p.k_pool_r : p.k_pool;
-  const uint16_t* const v_pool = second_store ? p.v_pool_r : p.v_pool;
   const int wg_hi = min(hi, P + wg_row_end);
   const int tile_begin = lo / kTileKeys;
   const int tile_end = (wg_hi + kTileKeys - 1) / kTileKeys;
@@ -243,7 +228,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     }
   }
 
-  const const_i32_ptr table = (const_i32_ptr)(second_store ? p.table_r : p.table);
+
   const int64_t head_stride = (int64_t)D * p.block_size;
   int k_src[LOADS], v_src[LOADS];
 #pragma unroll
@@ -256,12 +241,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   }
   auto issue_seq = [&](int i) __attribute__((always_inline)) {
     const int t = seq_tile(i);
+    // Tiles [remote_begin, remote_end) live in the second store.
+    const bool remote = t >= p.remote_begin && t < p.remote_end;
+    const const_i32_ptr table = (const_i32_ptr)(remote ? p.table_r : p.table);
     const int pos0 = t * kTileKeys;
     const int lb = pos0 / p.block_size;
     const int slot0 = pos0 - lb * p.block_size;
     const int64_t base = ((int64_t)table[lb] * p.h_kv + item.kv_head) * head_stride;
-    const uint16_t* kb = k_pool + base + (int64_t)slot0 * D;
-    const uint16_t* vb = v_pool + base + slot0;
+    const uint16_t* kb = (remote ? p.k_pool_r : p.k_pool) + base + (int64_t)slot0 * D;
+    const uint16_t* vb = (remote ? p.v_pool_r : p.v_pool) + base + slot0;
     uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     uint16_t* vl = kl + K_ELEMS;
 #pragma unroll

@@ -18,13 +18,11 @@ constexpr int kGroupThreads = 64 * kWavesPerGroup;
 // query heads of one GQA group times `32 * 8 / heads_per_wg` query rows, for
 // one KV range.
 //
-// KV ranges, in order: `parts_before` ranges cutting tiles [0, remote_begin)
-// (first store), `parts_remote` ranges cutting tiles [remote_begin,
-// remote_end) (second store), the remaining n_ranges - 1 - parts_before -
-// parts_remote ranges cutting tiles [remote_end, ceil(P / 64)) (first store;
-// the last one ends at P), then the chunk's own keys [P, P + L) (first
-// store).  Tile t holds keys [64 t, 64 t + 64).  n_ranges == 1 is the
-// unsplit launch over [0, P + L) from the first store.
+// KV ranges: n_ranges == 1 is the unsplit launch over [0, P + L); otherwise
+// n_ranges - 1 ranges cut the prefix tiles [0, ceil(P / 64)) evenly (the
+// last one ends at P), then the chunk's own keys [P, P + L).  Tile t holds
+// keys [64 t, 64 t + 64); tiles [remote_begin, remote_end) are read from the
+// second store, every other tile from the first.
 struct AttnLaunch {
   const uint16_t* q;        // bf16 [L][Hq][D]
   const uint16_t* k_pool;   // bf16 [nb][Hkv][bs][D]
@@ -49,8 +47,6 @@ struct AttnLaunch {
   int32_t n_ranges;         // 1 = unsplit; else prefix ranges + 1 chunk range
   int32_t remote_begin;     // tiles [remote_begin, remote_end) live in the second store
   int32_t remote_end;
-  int32_t parts_before;     // ranges over tiles [0, remote_begin)
-  int32_t parts_remote;     // ranges over the second store's tiles
   int32_t total_wgs;
   float scale_log2;         // scale * log2(e)
 };

@@ -170,7 +170,7 @@ def attn2(mocap_lib, kv=None, table=FAKE, n_table=64, rkv=None, rtable=FAKE, n_r
     (dict(rkv="dim"), INVALID),
     (dict(scale=0.0), INVALID),
     (dict(n_table=4), INVALID),
-    (dict(splits=1), WORKSPACE),                   # a remote range always splits
+    (dict(splits=3), WORKSPACE),                   # a split plan without workspace
 ])
 def test_two_store_rejects(mocap_lib, kwargs, expect):
     variants = {"h_kv": dict(h_kv=4), "block": dict(block_size=128), "dim": dict(head_dim=64)}
@@ -188,19 +188,10 @@ def test_two_store_empty_remote_range_is_single_store(mocap_lib):
 def test_two_store_workspace_size(mocap_lib):
     ws2 = mocap_lib.mocap_chunk_attn_two_store_workspace_size
     ws = mocap_lib.mocap_chunk_attn_workspace_size
-
-    def nbytes(r):
-        rows = r * 32 * 256
-        return rows * 128 * 4 + rows * 4
-
-    # P = 4096 (64 tiles), L = 256.  Remote in the middle: three segments.
-    assert ws2(4096, 256, 32, 8, 128, 1024, 2048, 1) == (4, nbytes(4))   # raised to 3 + 1
-    assert ws2(4096, 256, 32, 8, 128, 1024, 2048, 10) == (10, nbytes(10))
-    assert ws2(4096, 256, 32, 8, 128, 0, 2048, 1) == (3, nbytes(3))      # remote first
-    assert ws2(4096, 256, 32, 8, 128, 2048, 4096, 2) == (3, nbytes(3))   # remote last
-    assert ws2(4096, 256, 32, 8, 128, 0, 4096, 1) == (2, nbytes(2))      # all remote
-    assert ws2(4096, 256, 32, 8, 128, 0, 4096, 500)[0] == 65             # one range per tile at most
-    assert ws2(4096, 256, 32, 8, 128, 1024, 1024, 5) == ws(4096, 256, 32, 8, 128, 5)
+    # The store is chosen per tile, so the plan is the single-store plan.
+    for rb, re in [(1024, 2048), (0, 2048), (2048, 4096), (0, 4096), (1024, 1024), (64, 128)]:
+        for splits in (1, 2, 5, 500):
+            assert ws2(4096, 256, 32, 8, 128, rb, re, splits) == ws(4096, 256, 32, 8, 128, splits)
     assert ws2(4096, 0, 32, 8, 128, 0, 1024, 0) == (1, 0)
     for bad in [(4096, 256, 32, 8, 128, 0, 4097, 0), (4096, 256, 32, 8, 128, 64, 0, 0),
                 (4096, 256, 32, 8, 128, 10, 64, 0)]:
