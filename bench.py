@@ -197,7 +197,7 @@ def main():
         "causal_flops_per_step": flops,
         "roofline": {
             "bound": "mfma",
-            "kernel": "chunk_attn_kernel<128>" if w.head_dim == 128 else "chunk_attn_kernel<64>",
+            "kernel": f"chunk_attn_kernel<{w.head_dim}, {'true' if runner.remote else 'false'}>",
             "achieved": round(achieved, 2),
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",

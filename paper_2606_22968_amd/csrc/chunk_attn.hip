@@ -154,7 +154,9 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
-template <int D>
+// TWO: some prefix tiles come from the second store (a separate
+// instantiation, so single-store launches carry no per-tile store choice).
+template <int D, bool TWO>
 __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnLaunch p) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int KS = D / 16;
@@ -242,7 +244,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   auto issue_seq = [&](int i) __attribute__((always_inline)) {
     const int t = seq_tile(i);
     // Tiles [remote_begin, remote_end) live in the second store.
-    const bool remote = t >= p.remote_begin && t < p.remote_end;
+    const bool remote = TWO && t >= p.remote_begin && t < p.remote_end;
     const const_i32_ptr table = (const_i32_ptr)(remote ? p.table_r : p.table);
     const int pos0 = t * kTileKeys;
     const int lb = pos0 / p.block_size;
@@ -522,10 +524,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 
 hipError_t launch_chunk_attn(const AttnLaunch& p, int head_dim, hipStream_t stream) {
   const dim3 grid(p.total_wgs), block(kAttnThreads);
+  const bool two = p.remote_end > p.remote_begin;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(chunk_attn_kernel<128>, grid, block, 0, stream, p);
+    if (two) {
+      hipLaunchKernelGGL((chunk_attn_kernel<128, true>), grid, block, 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((chunk_attn_kernel<128, false>), grid, block, 0, stream, p);
+    }
   } else {
-    hipLaunchKernelGGL(chunk_attn_kernel<64>, grid, block, 0, stream, p);
+    if (two) {
+      hipLaunchKernelGGL((chunk_attn_kernel<64, true>), grid, block, 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((chunk_attn_kernel<64, false>), grid, block, 0, stream, p);
+    }
   }
   return hipGetLastError();
 }
