@@ -11,15 +11,16 @@
 //     share one KV head (GQA packing), so each K/V tile staged in LDS serves
 //     every query head of the group.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
-//     (global_load_lds_dwordx4, no staging registers) into a 5-stage ring
+//     (buffer_load_dwordx4 ... lds, no staging registers) into a 5-stage ring
 //     (160 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
 //     barrier per tile.  Waves 4-7 meet each barrier after their scores, half
 //     a tile behind waves 0-3, so one wave's score MFMAs overlap the other's
 //     softmax on each SIMD.
 //   * Software pipelining inside each wavefront: tile k's scores are followed
-//     by tile k-1's P*V product and tile k's exp/pack work in one basic block,
-//     so the MFMAs of one tile and the VALU work of the next issue side by
-//     side.  The probabilities alternate between two register buffers.
+//     by tile k-1's P*V product with tile k's exp/pack/row-sum work woven in
+//     at a fixed ratio (two scores per MFMA), so the matrix and vector units
+//     work side by side.  The probabilities alternate between two register
+//     buffers.  LDS operand fragments are read two or more MFMAs ahead.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane's accumulator then holds one query and
 //     16 keys, so row statistics need one cross-half exchange
@@ -32,10 +33,10 @@
 //     maxima (see the bookkeeping note below); the row sum adds the bf16
 //     probabilities with v_dot2, so numerator and denominator agree.
 //   * Only tiles that straddle the causal diagonal or a range edge are
-//     masked (a per-lane bit mask applied to the packed probabilities); tiles
-//     entirely above the diagonal are never visited.  Keys at or beyond P+L
-//     (unwritten store memory) are zero-filled in LDS so a masked probability
-//     of 0 never meets a NaN.
+//     masked (their hidden scores are set to -inf before the exponentials);
+//     tiles entirely above the diagonal are never visited.  Keys at or beyond
+//     P+L (unwritten store memory) are zero-filled in LDS so a probability of
+//     0 never meets a NaN.
 //   * Optional split of the prefix into ranges: each range writes normalised
 //     fp32 partials and their log-sum-exp; lse_merge.hip combines them.
 //   * A run of prefix tiles may come from a second store (a debtor stage's
@@ -119,6 +120,8 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
 constexpr float kSumLimit = 1152921504606846976.0f;  // 2^60
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// Word 3 of a raw (untyped) buffer descriptor: 32-bit data format.
+constexpr int kBufferWord3 = 0x00020000;
 typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
 
 // LDS layout of one stage (no padding; 16-byte chunks XOR-swizzled).  A
@@ -136,10 +139,20 @@ __device__ __forceinline__ int k_swizzle(int r) {
 }
 __device__ __forceinline__ int v_swizzle(int e) { return (e >> 1) & 7; }
 
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// s_waitcnt immediates in the gfx9 encoding (vmcnt in bits 3:0 and 15:14,
+// expcnt in 6:4, lgkmcnt in 11:8).  Written as builtins, not inline
+// assembly, so the compiler's own wait insertion knows what has completed.
+constexpr int kWaitLgkm0 = 0xC07F;
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __builtin_amdgcn_s_barrier();
+}
 
 template <int N>
-__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -175,7 +188,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar registers
   const int half = lane >> 5;
   const int l32 = lane & 31;
 
@@ -254,11 +267,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     const uint16_t* vb = (remote ? p.v_pool_r : p.v_pool) + base + slot0;
     uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     uint16_t* vl = kl + K_ELEMS;
+    // Buffer loads rather than global_load_lds: while a global (FLAT-encoded)
+    // LDS copy is in flight, the compiler's wait insertion cannot count LDS
+    // reads one by one and waits for all of them before each MFMA.
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc((void*)kb, 0, -1, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, -1, kBufferWord3);
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int dst = (j * kAttnWaves + wave) * 64 * 8;
-      __builtin_amdgcn_global_load_lds(kb + k_src[j], (lds_ptr_t)(kl + dst), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vb + v_src[j], (lds_ptr_t)(vl + dst), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(kl + dst), 16, k_src[j] * 2, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(vl + dst), 16, v_src[j] * 2, 0, 0, 0);
     }
   };
   auto publish_seq = [&](int i, int later) __attribute__((always_inline)) {
@@ -288,8 +306,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   float m_run = -INFINITY, l_run = 0.f, m_cand = -INFINITY;
   bool rerun = false;
   const float sl2 = p.scale_log2;
-  const int k_row_lo = key_row_order(l32);
-  const int v_row_sw = v_swizzle(l32);
+  int k_row_lo = key_row_order(l32);
+  int v_row_sw = v_swizzle(l32);
   const uint32_t ones = 0x3F803F80u;
 
   auto visible_bits = [&](int base) __attribute__((always_inline)) -> uint32_t {
@@ -303,7 +321,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // Pieces of one 64-key tile: scores (16 MFMAs), probabilities of each
   // 32-key half (VALU), settle, P*V (16 MFMAs).
   f32x16 s[2];
-  uint32_t vis[2] = {0xFFFFu, 0xFFFFu};
   uint32_t pk[2][2][8];  // [buffer][32-key half][packed pairs]: tile i uses buffer i % 2
   float rs[2];
   auto scores = [&](int i, bool masked) __attribute__((always_inline)) {
@@ -331,17 +348,30 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[ks], qf[ks], s[0], 0, 0, 0);
       s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], qf[ks], s[1], 0, 0, 0);
     }
-    vis[0] = vis[1] = 0xFFFFu;
+    // Issue order: four fragment reads, then each MFMA followed by the next
+    // read, so reads stay two k-steps ahead of their MFMAs.
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);  // LDS reads
+#pragma unroll
+    for (int k = 0; k < 2 * KS; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // MFMA
+      if (k + 4 < 2 * KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+    }
     if (masked) {
+      // Hidden scores become -inf, so their probabilities are exactly 0.
       const int tstart = seq_tile(i) * kTileKeys;
-      vis[0] = visible_bits(tstart + half * 8);
-      vis[1] = visible_bits(tstart + 32 + half * 8);
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        const uint32_t vm = visible_bits(tstart + sb * 32 + half * 8);
+#pragma unroll
+        for (int i2 = 0; i2 < 16; ++i2) {
+          const int keep = __builtin_amdgcn_sbfe((int)vm, i2, 1);
+          s[sb][i2] = __int_as_float((__float_as_int(s[sb][i2]) & keep) | (~keep & (int)0xFF800000u));
+        }
+      }
     }
   };
-  // Probabilities of both 32-key halves into buffer b: exponentials and
-  // packing first (one straight run of VALU work), then the mask of a
-  // straddling tile, then the row sums.
-  auto probs = [&](int b, bool masked, float neg_m) __attribute__((always_inline)) {
+  // Probabilities of both 32-key halves into buffer b and their row sums.
+  auto probs = [&](int b, float neg_m) __attribute__((always_inline)) {
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -350,19 +380,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
         pk[b][sb][i2 / 2] = pack_bf16x2(e0, e1);
       }
-    if (masked) {
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        uint32_t vm = vis[sb];
-        asm volatile("" : "+v"(vm));  // keeps the per-pair masks from being computed early
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t lo_half = (uint32_t)__builtin_amdgcn_sbfe((int)vm, 2 * j, 1);
-          const uint32_t hi_half = (uint32_t)__builtin_amdgcn_sbfe((int)vm, 2 * j + 1, 1);
-          pk[b][sb][j] &= (lo_half & 0x0000FFFFu) | (hi_half & 0xFFFF0000u);
-        }
-      }
-    }
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
       float acc = 0.f;
@@ -371,23 +388,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       rs[sb] = acc;
     }
   };
+  // A row still without a reference exponent (m = -inf, exponent offset
+  // +inf) has an infinite or NaN sum here, which sends it to the fresh branch.
   auto settle = [&](int b) __attribute__((always_inline)) {
     const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
       const bool row_over = lane_pair_max(over ? 1.f : 0.f) > 0.f;
-      // The visibility masks pass through an empty asm statement here, so the
-      // compiler cannot hoist this rare path's per-element bit selects into
-      // the main loop (where they would hold registers).
-      asm volatile("" : "+v"(vis[0]), "+v"(vis[1]));
-      // Largest visible score of the block: invisible ones read as -inf.
+      // Largest score of the block (hidden ones are -inf).
       float mx = -INFINITY;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int i2 = 0; i2 < 16; ++i2) {
-          const int keep = __builtin_amdgcn_sbfe((int)vis[sb], i2, 1);
-          mx = fmaxf(mx, __int_as_float((__float_as_int(s[sb][i2]) & keep) | (~keep & (int)0xFF800000u)));
-        }
+        for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, s[sb][i2]);
       mx = lane_pair_max(mx) * sl2;
       const bool fresh = lane_pair_sum(l_run) == 0.f;
       if (row_over && !fresh) {
@@ -397,7 +409,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       if (row_over && fresh) {
         m_run = mx;
         const float nm = m_run == -INFINITY ? 0.f : -m_run;
-        probs(b, true, nm);
+        probs(b, nm);
       }
     }
     l_run += rs[0] + rs[1];
@@ -418,6 +430,43 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kst, md), pb, oacc[md], 0, 0, 0);
     }
   };
+  // Tile i's P*V (probabilities from buffer bo) with the next tile's
+  // probabilities (into buffer bn) woven in: after each MFMA, the
+  // exponentials, packing and row sums of 32 / (4 * MD) score pairs.  V
+  // fragments are read two MFMAs ahead.  The scheduling barrier after each
+  // step keeps this order, which the compiler's scheduler would otherwise
+  // collapse into all MFMAs first.
+  auto pv_probs = [&](int i, int bo, int bn, float neg_m) __attribute__((always_inline)) {
+    const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
+    auto vfrag = [&](int kst, int md) __attribute__((always_inline)) {
+      const int vchunk = (kst * 2 + half) ^ v_row_sw;
+      return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
+    };
+    constexpr int NF = 4 * MD, AHEAD = 2, PAIRS = 16 / NF;
+    bf16x8 vf[AHEAD + 1];
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) vf[k] = vfrag(k / MD, k % MD);
+    float acc[2] = {0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < NF; ++k) {
+      const int kst = k / MD, md = k % MD, sb = kst / 2, kk = kst % 2;
+      if (k + AHEAD < NF) vf[(k + AHEAD) % (AHEAD + 1)] = vfrag((k + AHEAD) / MD, (k + AHEAD) % MD);
+      const bf16x8 pb = __builtin_bit_cast(
+          bf16x8, u32x4{pk[bo][sb][kk * 4], pk[bo][sb][kk * 4 + 1], pk[bo][sb][kk * 4 + 2], pk[bo][sb][kk * 4 + 3]});
+      oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k % (AHEAD + 1)], pb, oacc[md], 0, 0, 0);
+#pragma unroll
+      for (int q = 0; q < PAIRS; ++q) {
+        const int pr = k * PAIRS + q, nsb = pr / 8, j = pr % 8;
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j], sl2, neg_m));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j + 1], sl2, neg_m));
+        pk[bn][nsb][j] = pack_bf16x2(e0, e1);
+        acc[nsb] = dot2_bf16(pk[bn][nsb][j], ones, acc[nsb]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    rs[0] = acc[0];
+    rs[1] = acc[1];
+  };
   // Barrier k publishes tile k and frees the stage of tile k-3, which tile
   // k+2 refills (5 stages).  Waves 0-3 meet it at the top of tile k, waves
   // 4-7 after their scores of tile k-1, so the two waves of a SIMD are half a
@@ -435,19 +484,22 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     barrier_k(0);
     scores(0, masked);
     if (group_b && n_tiles > 1) barrier_k(1);
-    probs(0, masked, -m_run);
+    probs(0, -m_run);
     settle(0);
   };
   auto next_tile = [&](int i, int b, bool masked) __attribute__((always_inline)) {
     if (!group_b) barrier_k(i);
     scores(i, masked);
     if (group_b && i + 1 < n_tiles) barrier_k(i + 1);
-    pv(i - 1, b ^ 1);
-    probs(b, masked, -m_run);
+    pv_probs(i - 1, b ^ 1, b, -m_run);
     settle(b);
   };
 
   for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
+    // Without this, values the first tile derives from these (its masks, its
+    // LDS addresses) are computed once before the pass loop and then occupy
+    // registers through every later tile.
+    asm volatile("" : "+s"(lo), "+s"(hi), "+v"(k_row_lo), "+v"(v_row_sw));
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
     if (n_fast > 0) {
