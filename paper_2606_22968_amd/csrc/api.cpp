@@ -18,6 +18,17 @@
 
 namespace {
 
+// Magic number and shift for unsigned division by an invariant d >= 1, valid
+// for dividends below 2^31: l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1,
+// and n / d = (umulhi(n, m) + n) >> l (Granlund and Montgomery, 1994, round-up
+// method; the sum cannot overflow 32 bits because umulhi(n, m) <= n < 2^31).
+void block_divider(uint32_t d, uint32_t* magic, int32_t* shift) {
+  int l = 0;
+  while ((1ull << l) < d) ++l;
+  *magic = (uint32_t)((((1ull << l) - d) << 32) / d + 1);
+  *shift = l;
+}
+
 using mocap::kTileKeys;
 using mocap::kAttnWaveRows;
 using mocap::kAttnWaves;
@@ -279,6 +290,7 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   p.heads_per_wg = plan.hp;
   p.row_groups = plan.row_groups;
   p.block_size = kv->block_size;
+  block_divider((uint32_t)kv->block_size, &p.block_magic, &p.block_shift);
   p.n_ranges = plan.n_ranges;
   p.remote_begin = (int32_t)plan.remote_begin;
   p.remote_end = (int32_t)plan.remote_end;

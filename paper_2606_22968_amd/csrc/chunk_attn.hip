@@ -15,7 +15,8 @@
 //     (160 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
 //     barrier per tile.  Waves 4-7 meet each barrier after their scores, half
 //     a tile behind waves 0-3, so one wave's score MFMAs overlap the other's
-//     softmax on each SIMD.
+//     softmax on each SIMD.  Even tiles are copied by waves 0-3 and odd tiles
+//     by waves 4-7, so each wave computes a tile's addresses every other tile.
 //   * Software pipelining inside each wavefront: tile k's scores are followed
 //     by tile k-1's P*V product with tile k's exp/pack/row-sum work woven in
 //     at a fixed ratio (two scores per MFMA), so the matrix and vector units
@@ -178,8 +179,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   constexpr int V_ROW_CHUNKS = kTileKeys / 8;
   constexpr int K_ELEMS = kTileKeys * D;
   constexpr int BUF_ELEMS = 2 * K_ELEMS;
-  constexpr int LOADS = K_ELEMS / 8 / kAttnThreads;
-  constexpr int TILE_OPS = 2 * LOADS;
+  // Tile t is copied by the four waves of group t & 1 (waves 0-3 or 4-7).
+  constexpr int LOADS = K_ELEMS / 8 / (kAttnThreads / 2);
   constexpr int STAGES = 5;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
@@ -245,22 +246,25 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 
 
   const int64_t head_stride = (int64_t)D * p.block_size;
+  const int my_group = wave >> 2;
+  const int gwave = wave & 3;  // wave within its group of four
   int k_src[LOADS], v_src[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int chunk = (j * kAttnWaves + wave) * 64 + lane;
+    const int chunk = (j * 4 + gwave) * 64 + lane;
     const int kr = chunk / K_ROW_CHUNKS, kc = (chunk % K_ROW_CHUNKS) ^ k_swizzle<D>(kr);
     k_src[j] = kr * D + kc * 8;
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ v_swizzle(vr);
     v_src[j] = vr * p.block_size + vc * 8;
   }
   auto issue_seq = [&](int i) __attribute__((always_inline)) {
+    if ((i & 1) != my_group) return;
     const int t = seq_tile(i);
     // Tiles [remote_begin, remote_end) live in the second store.
     const bool remote = TWO && t >= p.remote_begin && t < p.remote_end;
     const const_i32_ptr table = (const_i32_ptr)(remote ? p.table_r : p.table);
     const int pos0 = t * kTileKeys;
-    const int lb = pos0 / p.block_size;
+    const int lb = (int)((__umulhi((uint32_t)pos0, p.block_magic) + (uint32_t)pos0) >> p.block_shift);
     const int slot0 = pos0 - lb * p.block_size;
     const int64_t base = ((int64_t)table[lb] * p.h_kv + item.kv_head) * head_stride;
     const uint16_t* kb = (remote ? p.k_pool_r : p.k_pool) + base + (int64_t)slot0 * D;
@@ -274,19 +278,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, -1, kBufferWord3);
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      const int dst = (j * kAttnWaves + wave) * 64 * 8;
+      const int dst = (j * 4 + gwave) * 64 * 8;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(kl + dst), 16, k_src[j] * 2, 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(vl + dst), 16, v_src[j] * 2, 0, 0, 0);
     }
   };
-  auto publish_seq = [&](int i, int later) __attribute__((always_inline)) {
-    if (later >= 2) {
-      wait_vmem<2 * TILE_OPS>();
-    } else if (later == 1) {
-      wait_vmem<TILE_OPS>();
-    } else {
-      wait_vmem<0>();
-    }
+  // The group that copied tile i waits for its copies (the only ones it has in
+  // flight: it copies its next tile only after this barrier); the other group
+  // has just the following tile in flight and does not wait.
+  auto publish_seq = [&](int i) __attribute__((always_inline)) {
+    if ((i & 1) == my_group) wait_vmem<0>();
     lds_barrier();
     const int tstart = seq_tile(i) * kTileKeys;
     if (tstart + kTileKeys > valid_end) {
@@ -472,7 +473,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // 4-7 after their scores of tile k-1, so the two waves of a SIMD are half a
   // tile apart.
   auto barrier_k = [&](int k) __attribute__((always_inline)) {
-    publish_seq(k, min(n_tiles - 1 - k, 1));
+    publish_seq(k);
     if (k + 2 < n_tiles) issue_seq(k + 2);
   };
   // Tile i: scores, then the previous tile's P*V (MFMA) in the same basic

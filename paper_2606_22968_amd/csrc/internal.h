@@ -44,6 +44,8 @@ struct AttnLaunch {
   int32_t heads_per_wg;     // 4, 2 or 1 (divides group)
   int32_t row_groups;       // ceil(L / rows_per_wg)
   int32_t block_size;
+  uint32_t block_magic;     // floor(n / block_size) = (umulhi(n, magic) + n) >> shift
+  int32_t block_shift;      //   for 0 <= n < 2^31 (division by an invariant integer)
   int32_t n_ranges;         // 1 = unsplit; else prefix ranges + 1 chunk range
   int32_t remote_begin;     // tiles [remote_begin, remote_end) live in the second store
   int32_t remote_end;

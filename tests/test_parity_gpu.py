@@ -45,6 +45,22 @@ def test_ragged_chunks_all_rows(gpu, oracle_lib, h_q, h_kv, d):
     check_chunks(oracle_lib, runner, q, k, v, scale, label=f"ragged {h_q}/{h_kv}/{d}")
 
 
+@pytest.mark.parametrize("block_size,h_q,h_kv,d,splits", [(192, 8, 2, 128, 0), (320, 8, 4, 64, 3),
+                                                          (448, 16, 4, 128, 2), (64 * 25, 4, 1, 128, 0)])
+def test_block_sizes_not_powers_of_two(gpu, oracle_lib, block_size, h_q, h_kv, d, splits):
+    # The kernel finds a position's block by multiply-and-shift division; a
+    # permuted table and NaN in unwritten slots catch a wrong block or slot.
+    lengths = [700, 129, 1000, 5, 64]
+    say(f"[case] block_size={block_size} h_q={h_q} h_kv={h_kv} d={d} splits={splits}")
+    q, k, v = synth.make_qkv(60 + block_size, sum(lengths), h_q, h_kv, d)
+    n_blocks = -(-sum(lengths) // block_size)
+    table = synth.permuted_table(n_blocks, 7 + block_size, pool_blocks=n_blocks + 3)
+    scale = d ** -0.5
+    runner = run_gpu(q, k, v, lengths, scale, block_size=block_size, table=table, pool_blocks=n_blocks + 3,
+                     num_splits=splits, pool_fill=float("nan"))
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"block_size={block_size}")
+
+
 @pytest.mark.parametrize("splits", [1, 2, 3, 7, 0])
 def test_forced_splits(gpu, oracle_lib, splits):
     lengths = [1500, 37, 600, 1]
