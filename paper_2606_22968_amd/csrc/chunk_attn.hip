@@ -11,12 +11,10 @@
 //     share one KV head (GQA packing), so each K/V tile staged in LDS serves
 //     every query head of the group.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
-//     (buffer_load_dwordx4 ... lds, no staging registers) into a 5-stage ring
-//     (160 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
-//     barrier per tile.  Waves 4-7 meet each barrier after their scores, half
-//     a tile behind waves 0-3, so one wave's score MFMAs overlap the other's
-//     softmax on each SIMD.  Even tiles are copied by waves 0-3 and odd tiles
-//     by waves 4-7, so each wave computes a tile's addresses every other tile.
+//     (buffer_load_dwordx4 ... lds, no staging registers) into a 4-stage ring
+//     (128 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
+//     barrier per tile.  Even tiles are copied by waves 0-3 and odd tiles by
+//     waves 4-7, so each wave computes a tile's addresses every other tile.
 //   * Software pipelining inside each wavefront: tile k's scores are followed
 //     by tile k-1's P*V product with tile k's exp/pack/row-sum work woven in
 //     at a fixed ratio (two scores per MFMA), so the matrix and vector units
@@ -181,7 +179,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   constexpr int BUF_ELEMS = 2 * K_ELEMS;
   // Tile t is copied by the four waves of group t & 1 (waves 0-3 or 4-7).
   constexpr int LOADS = K_ELEMS / 8 / (kAttnThreads / 2);
-  constexpr int STAGES = 5;
+  constexpr int STAGES = 4;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
   // Between passes no tile is in flight, so the re-run vote borrows LDS.
@@ -468,30 +466,26 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     rs[0] = acc[0];
     rs[1] = acc[1];
   };
-  // Barrier k publishes tile k and frees the stage of tile k-3, which tile
-  // k+2 refills (5 stages).  Waves 0-3 meet it at the top of tile k, waves
-  // 4-7 after their scores of tile k-1, so the two waves of a SIMD are half a
-  // tile apart.
+  // Barrier k, met by every wave at the top of tile k, publishes tile k and
+  // frees the stage of tile k-2 (every wave has finished its P*V), which tile
+  // k+2 refills.
   auto barrier_k = [&](int k) __attribute__((always_inline)) {
     publish_seq(k);
     if (k + 2 < n_tiles) issue_seq(k + 2);
   };
-  // Tile i: scores, then the previous tile's P*V (MFMA) in the same basic
-  // block as this tile's probabilities (VALU), so one wave keeps both the
-  // matrix and the vector units busy; the probabilities alternate between
-  // two buffers.  Tile 0 has no predecessor.
-  const bool group_b = wave >= 4;
+  // Tile i: scores, then the previous tile's P*V with this tile's
+  // probabilities woven in, so one wave keeps both the matrix and the vector
+  // units busy; the probabilities alternate between two buffers.  Tile 0 has
+  // no predecessor.
   auto first_tile = [&](bool masked) __attribute__((always_inline)) {
     barrier_k(0);
     scores(0, masked);
-    if (group_b && n_tiles > 1) barrier_k(1);
     probs(0, -m_run);
     settle(0);
   };
   auto next_tile = [&](int i, int b, bool masked) __attribute__((always_inline)) {
-    if (!group_b) barrier_k(i);
+    barrier_k(i);
     scores(i, masked);
-    if (group_b && i + 1 < n_tiles) barrier_k(i + 1);
     pv_probs(i - 1, b ^ 1, b, -m_run);
     settle(b);
   };
