@@ -108,3 +108,34 @@ def test_score_far_above_first_block_reruns(gpu, oracle_lib, target):
     scale = 128 ** -0.5
     runner = run_gpu(q, k, v, lengths, scale)
     check_chunks(oracle_lib, runner, q, k, v, scale, label=f"overflow re-run ({target})")
+
+
+def _random_config(index):
+    """Seeded random shape: heads, head_dim, block size, chunk lengths, table
+    and split count drawn independently (at most ~2500 tokens, 32 query heads)."""
+    import random
+    rng = random.Random(9000 + index)
+    h_kv = rng.choice([1, 2, 4, 8])
+    g = rng.choice([1, 2, 3, 4, 8])
+    while h_kv * g > 32:
+        g //= 2
+    d = rng.choice([64, 128])
+    block_size = rng.choice([64, 128, 192, 256, 320])
+    lengths = [rng.choice([1, rng.randint(2, 63), rng.randint(64, 700)]) for _ in range(rng.randint(1, 6))]
+    permuted = rng.random() < 0.5
+    splits = rng.choice([0, 0, 1, 2, 3, 5])
+    return h_kv * g, h_kv, d, block_size, lengths, permuted, splits
+
+
+@pytest.mark.parametrize("index", range(24))
+def test_random_configs_all_rows(gpu, oracle_lib, index):
+    h_q, h_kv, d, block_size, lengths, permuted, splits = _random_config(index)
+    say(f"[case] random #{index}: h_q={h_q} h_kv={h_kv} d={d} bs={block_size} lengths={lengths} "
+        f"permuted={permuted} splits={splits}")
+    q, k, v = synth.make_qkv(500 + index, sum(lengths), h_q, h_kv, d)
+    n_blocks = -(-sum(lengths) // block_size)
+    table = synth.permuted_table(n_blocks, 77 + index, pool_blocks=n_blocks + 2) if permuted else None
+    scale = 0.7 * d ** -0.5
+    runner = run_gpu(q, k, v, lengths, scale, block_size=block_size, table=table,
+                     pool_blocks=(n_blocks + 2) if permuted else None, num_splits=splits, pool_fill=float("nan"))
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"random #{index}")
