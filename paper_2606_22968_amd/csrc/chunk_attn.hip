@@ -17,9 +17,10 @@
 //     waves 4-7, so each wave computes a tile's addresses every other tile.
 //   * Software pipelining inside each wavefront: tile k's scores are followed
 //     by tile k-1's P*V product with tile k's exp/pack/row-sum work woven in
-//     at a fixed ratio (two scores per MFMA), so the matrix and vector units
-//     work side by side.  The probabilities alternate between two register
-//     buffers.  LDS operand fragments are read two or more MFMAs ahead.
+//     at a fixed ratio (two scores per MFMA, four at head_dim 64), so the
+//     matrix and vector units work side by side.  The probabilities alternate
+//     between two register buffers.  LDS operand fragments are read two or
+//     more MFMAs ahead.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane's accumulator then holds one query and
 //     16 keys, so row statistics need one cross-half exchange
@@ -445,7 +446,23 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     bf16x8 vf[AHEAD + 1];
 #pragma unroll
     for (int k = 0; k < AHEAD; ++k) vf[k] = vfrag(k / MD, k % MD);
+    // Within the weave, a pair's pack trails its exponentials by two pairs
+    // and its row-sum step by four, so no VALU instruction waits on the one
+    // just before it.
+    constexpr int LAG_PACK = 2, LAG_SUM = 4;
     float acc[2] = {0.f, 0.f};
+    float ex[16][2];
+    auto do_exp = [&](int pr) __attribute__((always_inline)) {
+      const int nsb = pr / 8, j = pr % 8;
+      ex[pr][0] = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j], sl2, neg_m));
+      ex[pr][1] = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j + 1], sl2, neg_m));
+    };
+    auto do_pack = [&](int pr) __attribute__((always_inline)) {
+      pk[bn][pr / 8][pr % 8] = pack_bf16x2(ex[pr][0], ex[pr][1]);
+    };
+    auto do_sum = [&](int pr) __attribute__((always_inline)) {
+      acc[pr / 8] = dot2_bf16(pk[bn][pr / 8][pr % 8], ones, acc[pr / 8]);
+    };
 #pragma unroll
     for (int k = 0; k < NF; ++k) {
       const int kst = k / MD, md = k % MD, sb = kst / 2, kk = kst % 2;
@@ -455,13 +472,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k % (AHEAD + 1)], pb, oacc[md], 0, 0, 0);
 #pragma unroll
       for (int q = 0; q < PAIRS; ++q) {
-        const int pr = k * PAIRS + q, nsb = pr / 8, j = pr % 8;
-        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j], sl2, neg_m));
-        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j + 1], sl2, neg_m));
-        pk[bn][nsb][j] = pack_bf16x2(e0, e1);
-        acc[nsb] = dot2_bf16(pk[bn][nsb][j], ones, acc[nsb]);
+        const int pr = k * PAIRS + q;
+        do_exp(pr);
+        if (pr >= LAG_PACK) do_pack(pr - LAG_PACK);
+        if (pr >= LAG_SUM) do_sum(pr - LAG_SUM);
       }
       __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int pr = 16; pr < 16 + LAG_SUM; ++pr) {
+      if (pr - LAG_PACK < 16) do_pack(pr - LAG_PACK);
+      do_sum(pr - LAG_SUM);
     }
     rs[0] = acc[0];
     rs[1] = acc[1];
