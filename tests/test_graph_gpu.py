@@ -16,12 +16,14 @@ def _all_lse(r):
     return torch.cat([r.lse(c).flatten() for c in range(len(r.lengths))])
 
 
-@pytest.mark.parametrize("splits", [0, 3])
-def test_graph_replay_equals_eager(gpu, splits):
-    lengths = [700, 1024, 333, 1500]
-    say(f"[case] graph capture, splits={splits}")
+@pytest.mark.parametrize("splits,remote", [(0, None), (3, None), (0, (0, 1664)), (2, (512, 1664))])
+def test_graph_replay_equals_eager(gpu, splits, remote):
+    # remote: the two-store call, with positions [begin, end) read from a
+    # second store (every chunk boundary inside the range is a multiple of 64).
+    lengths = [704, 1024, 333, 1500]
+    say(f"[case] graph capture, splits={splits} remote={remote}")
     q, k, v = (t.cuda() for t in synth.make_qkv(81, sum(lengths), 32, 8, 128))
-    r = ChunkedPrefill(32, 8, 128, lengths, num_splits=splits)
+    r = ChunkedPrefill(32, 8, 128, lengths, num_splits=splits, remote=remote)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -38,6 +40,9 @@ def test_graph_replay_equals_eager(gpu, splits):
         r._lse_flat.fill_(float("nan"))
         r.store.k_pool.fill_(float("nan"))
         r.store.v_pool.fill_(float("nan"))
+        if r.remote_store is not None:
+            r.remote_store.k_pool.fill_(float("nan"))
+            r.remote_store.v_pool.fill_(float("nan"))
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
