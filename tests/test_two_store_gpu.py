@@ -122,3 +122,40 @@ def test_two_store_full_size_half_remote(gpu, oracle_lib):
     e = (single.o.double() - o_two.double()).abs()
     say(f"[compare] two-store vs single: O max {e.max().item():.3e} mean {e.mean().item():.3e}")
     assert e.max().item() <= 2e-2 and e.mean().item() <= 2e-3
+
+
+def _random_two_store(index):
+    """Seeded random two-store case: chunk lengths in whole tiles (the last
+    one ragged), a tile-aligned remote range, random heads, head_dim, block
+    size, tables and split count."""
+    import random
+    rng = random.Random(7000 + index)
+    h_kv = rng.choice([1, 2, 4])
+    h_q = h_kv * rng.choice([1, 2, 4])
+    d = rng.choice([64, 128])
+    block_size = rng.choice([64, 128, 192, 256])
+    lengths = [64 * rng.randint(1, 10) for _ in range(rng.randint(2, 5))] + [rng.randint(1, 200)]
+    tiles = sum(lengths[:-1]) // 64
+    b = rng.randint(0, tiles - 1)
+    e = rng.randint(b + 1, tiles)
+    splits = rng.choice([0, 0, 1, 3])
+    permuted = rng.random() < 0.5
+    return h_q, h_kv, d, block_size, lengths, (64 * b, 64 * e), splits, permuted
+
+
+@pytest.mark.parametrize("index", range(12))
+def test_two_store_random_configs_all_rows(gpu, oracle_lib, index):
+    h_q, h_kv, d, block_size, lengths, remote, splits, permuted = _random_two_store(index)
+    S = sum(lengths)
+    say(f"[case] two-store random #{index}: h_q={h_q} h_kv={h_kv} d={d} bs={block_size} lengths={lengths} "
+        f"remote={remote} splits={splits} permuted={permuted}")
+    q, k, v = synth.make_qkv(600 + index, S, h_q, h_kv, d)
+    kw = dict(block_size=block_size, remote=remote, num_splits=splits, pool_fill=NAN)
+    if permuted:
+        n_blocks = -(-S // block_size)
+        n_remote = -(-remote[1] // block_size)
+        kw.update(table=synth.permuted_table(n_blocks, 80 + index, n_blocks + 3), pool_blocks=n_blocks + 3,
+                  remote_table=synth.permuted_table(n_remote, 90 + index, n_remote + 2))
+    scale = d ** -0.5
+    r = _run(q, k, v, lengths, scale, **kw)
+    check_chunks(oracle_lib, r, q, k, v, scale, label=f"two-store random #{index}")
