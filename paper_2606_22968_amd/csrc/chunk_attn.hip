@@ -30,8 +30,11 @@
 //     probabilities of a P*V step belong to 8 consecutive keys, which are 16
 //     contiguous bytes of the key-contiguous V layout.
 //   * Softmax in base 2 with scale*log2(e) folded into one FMA, without block
-//     maxima (see the bookkeeping note below); the row sum adds the bf16
-//     probabilities with v_dot2, so numerator and denominator agree.
+//     maxima (see the bookkeeping note below).  Each row keeps two sums: the
+//     bf16 probabilities that feed P*V (added with v_dot2), which normalise O
+//     so numerator and denominator agree, and the fp32 exponentials before
+//     rounding, which give the log-sum-exp (a bf16 sum would carry the 2^-8
+//     rounding of a dominant probability into the LSE).
 //   * Only tiles that straddle the causal diagonal or a range edge are
 //     masked (their hidden scores are set to -inf before the exponentials);
 //     tiles entirely above the diagonal are never visited.  Keys at or beyond
@@ -303,7 +306,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   f32x16 oacc[MD];
 #pragma unroll
   for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f, m_cand = -INFINITY;
+  // l_run: sum of the bf16 probabilities (normalises O); f_run: sum of the
+  // fp32 exponentials (the log-sum-exp).
+  float m_run = -INFINITY, l_run = 0.f, f_run = 0.f, m_cand = -INFINITY;
   bool rerun = false;
   const float sl2 = p.scale_log2;
   int k_row_lo = key_row_order(l32);
@@ -322,7 +327,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // 32-key half (VALU), settle, P*V (16 MFMAs).
   f32x16 s[2];
   uint32_t pk[2][2][8];  // [buffer][32-key half][packed pairs]: tile i uses buffer i % 2
-  float rs[2];
+  float rs[2], fs[2];  // per 32-key half: bf16 sum, fp32 sum
   auto scores = [&](int i, bool masked) __attribute__((always_inline)) {
     const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     const uint16_t* krow0 = kl + k_row_lo * D;
@@ -373,13 +378,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // Probabilities of both 32-key halves into buffer b and their row sums.
   auto probs = [&](int b, float neg_m) __attribute__((always_inline)) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+    for (int sb = 0; sb < 2; ++sb) {
+      float fa = 0.f;
 #pragma unroll
       for (int i2 = 0; i2 < 16; i2 += 2) {
         const float e0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, neg_m));
         const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
         pk[b][sb][i2 / 2] = pack_bf16x2(e0, e1);
+        fa += e0 + e1;
       }
+      fs[sb] = fa;
+    }
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
       float acc = 0.f;
@@ -413,6 +422,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       }
     }
     l_run += rs[0] + rs[1];
+    f_run += fs[0] + fs[1];
   };
   auto pv = [&](int i, int b) __attribute__((always_inline)) {
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
@@ -450,7 +460,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     // and its row-sum step by four, so no VALU instruction waits on the one
     // just before it.
     constexpr int LAG_PACK = 2, LAG_SUM = 4;
-    float acc[2] = {0.f, 0.f};
+    float acc[2] = {0.f, 0.f}, facc[2] = {0.f, 0.f};
     float ex[16][2];
     auto do_exp = [&](int pr) __attribute__((always_inline)) {
       const int nsb = pr / 8, j = pr % 8;
@@ -462,6 +472,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     };
     auto do_sum = [&](int pr) __attribute__((always_inline)) {
       acc[pr / 8] = dot2_bf16(pk[bn][pr / 8][pr % 8], ones, acc[pr / 8]);
+      facc[pr / 8] += ex[pr][0] + ex[pr][1];
     };
 #pragma unroll
     for (int k = 0; k < NF; ++k) {
@@ -486,6 +497,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     }
     rs[0] = acc[0];
     rs[1] = acc[1];
+    fs[0] = facc[0];
+    fs[1] = facc[1];
   };
   // Barrier k, met by every wave at the top of tile k, publishes tile k and
   // frees the stage of tile k-2 (every wave has finished its P*V), which tile
@@ -545,6 +558,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     m_run = fmaxf(m_run, m_cand);
     m_cand = -INFINITY;
     l_run = 0.f;
+    f_run = 0.f;
 #pragma unroll
     for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
     rerun = false;
@@ -552,10 +566,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 
   const bool split = p.n_ranges > 1;
   const float l_tot = lane_pair_sum(l_run);
+  const float f_tot = lane_pair_sum(f_run);
   const int row = row0 + l32;
   if (row < L) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float row_lse = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+    const float row_lse = f_tot > 0.f ? (m_run + log2f(f_tot)) * kLn2 : -INFINITY;
     if (!split) {
       uint16_t* orow = p.o + ((int64_t)row * p.h_q + head) * D;
 #pragma unroll

@@ -13,13 +13,12 @@ from paper_2606_22968_amd.prefill import ChunkedPrefill
 # against the fp64 oracle.
 O_MAX_ABS = 2e-2
 O_MEAN_ABS = 2e-3
-# LSE bar, derived from the arithmetic (no bar is stated for it): the row sum
-# adds the bf16-rounded probabilities that also feed P*V.  bf16 keeps 8
-# significant bits, so each rounded probability is within 2^-8 relative of
-# the exact one, the sum is within 2^-8 relative, and
-# |delta LSE| <= ln(1 + 2^-8) / (1 - 2^-8) ~= 3.91e-3 (reached when one key
-# dominates a row); fp32 exp and accumulation add terms of order 1e-5.
-LSE_MAX_ABS = 4e-3
+# LSE bar (no bar is stated for it): max-abs 1e-3 in natural-log units.  The
+# kernel takes the log-sum-exp from fp32 sums of the unrounded exponentials
+# (fp32 exp2 and accumulation: relative errors of order 1e-6 on ordinary rows);
+# the bf16 rounding of the probabilities only enters O, whose normaliser sums
+# the same rounded values that feed P*V.
+LSE_MAX_ABS = 1e-3
 
 
 def say(msg):
