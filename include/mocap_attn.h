@@ -318,6 +318,42 @@ mocap_status mocap_lbcp_refine(int64_t seq_len, int32_t num_chunks, int32_t num_
                                const double* chunk_cost, double temp0, double temp_min, double alpha,
                                int32_t rounds, uint64_t seed, int32_t* lengths_inout, double* latency_out);
 
+/*
+ * Bytes of the library's static device scratch used by
+ * mocap_chunk_attn_noalloc (128 MiB, held on every device the library runs
+ * on until the process ends).
+ */
+#define MOCAP_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/*
+ * mocap_chunk_attn_noalloc -- mocap_chunk_attn without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  The
+ * split partials live in a static device array of MOCAP_NOALLOC_SCRATCH_BYTES
+ * inside the library; the call allocates nothing (no hipMalloc, no hipFree,
+ * no allocating library routine) and enqueues only kernel launches.
+ *
+ * Arguments, outputs and errors as in mocap_chunk_attn.  With num_splits = 0
+ * the plan is the best automatic plan whose partials fit the scratch (the
+ * same plan as mocap_chunk_attn's whenever that one fits); a requested
+ * num_splits whose partials need more than MOCAP_NOALLOC_SCRATCH_BYTES
+ * (see mocap_chunk_attn_workspace_size) returns MOCAP_ERR_WORKSPACE and
+ * launches nothing.  For the same plan the results are bitwise equal to
+ * mocap_chunk_attn's.
+ *
+ * Every call on a device shares that device's scratch, which keeps the last
+ * call's contents (nothing needs clearing: every partial a call reads is
+ * written earlier by the same call).  Calls that overlap on one device --
+ * on different streams, or from different threads without ordering -- race
+ * on the scratch; order them on one stream.  The first call on a device
+ * looks up the scratch's device address (hipGetSymbolAddress) with that
+ * device current; a failure returns MOCAP_ERR_HIP.
+ */
+mocap_status mocap_chunk_attn_noalloc(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                                      const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                      int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                                      int32_t num_splits, void* stream);
+
 /* A static, human-readable name for a status code. */
 const char* mocap_status_string(mocap_status status);
 

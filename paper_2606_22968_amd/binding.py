@@ -21,11 +21,15 @@ MOCAP_ERR_UNSUPPORTED = 2
 MOCAP_ERR_WORKSPACE = 3
 MOCAP_ERR_HIP = 4
 
+# MOCAP_NOALLOC_SCRATCH_BYTES: the static device scratch of mocap_chunk_attn_noalloc.
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
 # Every entry point the header declares.
 EXPORTED = (
     "mocap_kv_append",
     "mocap_chunk_attn_workspace_size",
     "mocap_chunk_attn",
+    "mocap_chunk_attn_noalloc",
     "mocap_chunk_attn_two_store",
     "mocap_chunk_attn_two_store_workspace_size",
     "mocap_chunk_plan",
@@ -83,6 +87,11 @@ def load_library():
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
         ctypes.c_int32, ctypes.c_void_p]
+    lib.mocap_chunk_attn_noalloc.restype = st
+    lib.mocap_chunk_attn_noalloc.argtypes = [
+        ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
     lib.mocap_chunk_attn_two_store.restype = st
     lib.mocap_chunk_attn_two_store.argtypes = [
         ctypes.POINTER(mocap_kv_store), ctypes.c_void_p, ctypes.c_int32,
@@ -212,6 +221,25 @@ def mocap_chunk_attn(store: KvStore, block_table: torch.Tensor, q: torch.Tensor,
         int(prefix_len), chunk_len, h_q, store.h_kv, head_dim, float(scale), o.data_ptr(),
         lse.data_ptr(), ws_ptr, ws_bytes, int(num_splits), _stream_handle(stream)),
         "mocap_chunk_attn")
+
+
+def mocap_chunk_attn_noalloc(store: KvStore, block_table: torch.Tensor, q: torch.Tensor, prefix_len: int,
+                             scale: float, o: torch.Tensor, lse: torch.Tensor, num_splits: int = 0,
+                             stream=None) -> None:
+    """mocap_chunk_attn with the split partials in the library's static device scratch."""
+    _require(block_table, torch.int32, "block_table", 1)
+    _require(q, torch.bfloat16, "q", 3)
+    _require(o, torch.bfloat16, "o", 3)
+    _require(lse, torch.float32, "lse", 2)
+    chunk_len, h_q, head_dim = q.shape
+    if o.shape != q.shape or tuple(lse.shape) != (h_q, chunk_len):
+        raise ValueError("o must match q and lse must be [h_q][chunk_len]")
+    desc = store.descriptor()
+    _check(load_library().mocap_chunk_attn_noalloc(
+        ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), q.data_ptr(),
+        int(prefix_len), chunk_len, h_q, store.h_kv, head_dim, float(scale), o.data_ptr(),
+        lse.data_ptr(), int(num_splits), _stream_handle(stream)),
+        "mocap_chunk_attn_noalloc")
 
 
 def mocap_chunk_attn_two_store_workspace_size(prefix_len: int, chunk_len: int, h_q: int, h_kv: int,

@@ -140,9 +140,10 @@ double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int he
 struct PlanKey {
   int64_t prefix_len;
   int32_t chunk_len, h_q, h_kv, head_dim, requested, slots;
+  size_t ws_cap;
   bool operator==(const PlanKey& o) const {
     return prefix_len == o.prefix_len && chunk_len == o.chunk_len && h_q == o.h_q && h_kv == o.h_kv &&
-           head_dim == o.head_dim && requested == o.requested && slots == o.slots;
+           head_dim == o.head_dim && requested == o.requested && slots == o.slots && ws_cap == o.ws_cap;
   }
 };
 
@@ -156,17 +157,19 @@ int g_plan_count = 0, g_plan_next = 0;
 
 // Number of KV ranges to use.  A requested count is clamped to what the
 // prefix allows; 0 picks, among the prefix cut into 1, 2, 4, 8 or 16 ranges
-// of at least 4 tiles (plus the chunk's own range), or no split at all, the
-// plan with the smallest modelled launch time.
+// of at least 4 tiles (plus the chunk's own range) whose workspace fits in
+// ws_cap bytes, or no split at all, the plan with the smallest modelled
+// launch time.
 int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int head_dim, int head_blocks_total,
-                  int row_groups, int rows_per_wg, int64_t prefix_tiles, int requested, int slots) {
+                  int row_groups, int rows_per_wg, int64_t prefix_tiles, int requested, int slots,
+                  size_t ws_cap) {
   if (prefix_tiles <= 0) return 1;
   if (requested >= 1) {
     if (requested == 1) return 1;
     const int64_t parts = requested - 1 < prefix_tiles ? requested - 1 : prefix_tiles;
     return (int)parts + 1;
   }
-  const PlanKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, requested, slots};
+  const PlanKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, requested, slots, ws_cap};
   {
     std::lock_guard<std::mutex> lock(g_plan_mutex);
     for (int i = 0; i < g_plan_count; ++i)
@@ -177,6 +180,7 @@ int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int 
                                       rows_per_wg, prefix_tiles, 1, slots);
   const int64_t max_parts = std::min<int64_t>(16, prefix_tiles / 4);
   for (int64_t parts = 1; parts <= max_parts; parts *= 2) {
+    if (workspace_for((int)parts + 1, chunk_len, h_q, head_dim) > ws_cap) break;
     const double us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
                                          rows_per_wg, prefix_tiles, (int)parts + 1, slots);
     if (us < best_us * 0.98) {  // a split must pay for itself clearly
@@ -193,7 +197,7 @@ int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int 
 }
 
 mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
-                       int32_t head_dim, int32_t num_splits, Plan* plan) {
+                       int32_t head_dim, int32_t num_splits, Plan* plan, size_t ws_cap = SIZE_MAX) {
   const int group = h_q / h_kv;
   plan->hp = heads_per_wg(group);
   const int rows_per_wg = kAttnWaveRows * (kAttnWaves / plan->hp);
@@ -208,7 +212,7 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
     if (st != MOCAP_OK) return st;
   }
   plan->n_ranges = choose_ranges(prefix_len, chunk_len, h_q, h_kv, head_dim, h_q / plan->hp, plan->row_groups,
-                                 rows_per_wg, plan->prefix_tiles, num_splits, cus);
+                                 rows_per_wg, plan->prefix_tiles, num_splits, cus, ws_cap);
   plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
   return MOCAP_OK;
 }
@@ -320,6 +324,33 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   return MOCAP_OK;
 }
 
+// ---- Scratch of the allocation-free entry point ----
+// Split partials of mocap_chunk_attn_noalloc live in this array: every device
+// the library runs on holds its own copy until the process ends.  Host code
+// never uses the array's name as an address: the device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+constexpr size_t kScratchBytes = MOCAP_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+mocap_status device_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOCAP_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MOCAP_ERR_UNSUPPORTED;
+  void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    ptr = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (ptr == nullptr) {
+      if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MOCAP_ERR_HIP;
+      g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return MOCAP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -397,6 +428,26 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
   if (st != MOCAP_OK) return st;
   return enqueue_attention(kv, block_table, nullptr, nullptr, plan, q, prefix_len, chunk_len, h_q, h_kv,
                            head_dim, scale, o, lse, workspace, workspace_bytes, stream);
+}
+
+mocap_status mocap_chunk_attn_noalloc(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
+                                      const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,
+                                      int32_t h_kv, int32_t head_dim, float scale, void* o, float* lse,
+                                      int32_t num_splits, void* stream) {
+  mocap_status st = check_attn_args(kv, block_table, n_table, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
+                                    scale, o, lse, num_splits);
+  if (st != MOCAP_OK || chunk_len == 0) return st;
+  Plan plan;
+  st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan, kScratchBytes);
+  if (st != MOCAP_OK) return st;
+  if (plan.ws_bytes > kScratchBytes) return MOCAP_ERR_WORKSPACE;  // a forced split that does not fit
+  void* ws = nullptr;
+  if (plan.n_ranges > 1) {
+    st = device_scratch(&ws);
+    if (st != MOCAP_OK) return st;
+  }
+  return enqueue_attention(kv, block_table, nullptr, nullptr, plan, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
+                           scale, o, lse, ws, kScratchBytes, stream);
 }
 
 mocap_status mocap_chunk_attn_two_store_workspace_size(int64_t prefix_len, int32_t chunk_len, int32_t h_q,

@@ -197,3 +197,54 @@ def test_two_store_workspace_size(mocap_lib):
                 (4096, 256, 32, 8, 128, 10, 64, 0)]:
         with pytest.raises(mocap_lib.MocapError):
             ws2(*bad)
+
+
+def noalloc(mocap_lib, kv=None, table=FAKE, n_table=64, q=FAKE, P=1024, L=256, h_q=32, h_kv=8, d=128,
+            scale=0.088, o=FAKE, lse=FAKE, splits=1):
+    lib = mocap_lib.load_library()
+    kv = store(mocap_lib) if kv is None else kv
+    ref = ctypes.byref(kv) if kv != "null" else None
+    return lib.mocap_chunk_attn_noalloc(ref, table, n_table, q, P, L, h_q, h_kv, d, scale, o, lse, splits, None)
+
+
+SCRATCH_BYTES = 128 << 20  # MOCAP_NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    assert "#define MOCAP_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)" in text
+
+
+@pytest.mark.parametrize("kwargs,expect", [
+    (dict(kv="null"), INVALID),
+    (dict(h_q=30), INVALID),
+    (dict(scale=math.nan), INVALID),
+    (dict(P=-1), INVALID),
+    (dict(n_table=4), INVALID),
+    (dict(q=MIS), INVALID),
+    (dict(lse=0), INVALID),
+    (dict(splits=-1), INVALID),
+    # A forced split whose partials exceed the scratch: P = 1M keys cut into
+    # 16 ranges + 1, L = 2048 rows of 32 heads at d 128 (~285 MB of partials).
+    (dict(P=1 << 20, L=2048, n_table=(1 << 20) // 256 + 8, splits=17), WORKSPACE),
+])
+def test_noalloc_rejects(mocap_lib, kwargs, expect):
+    assert noalloc(mocap_lib, **kwargs) == expect
+
+
+def test_noalloc_forced_split_just_over_the_scratch(mocap_lib):
+    # Forced 8-range plans of L rows x 32 heads at d 128 around the cap: every
+    # plan whose workspace (as mocap_chunk_attn_workspace_size reports it)
+    # exceeds MOCAP_NOALLOC_SCRATCH_BYTES is rejected with WORKSPACE before
+    # anything is launched.  (Plans that fit would launch, so they are left to
+    # the GPU test.)
+    ws = mocap_lib.mocap_chunk_attn_workspace_size
+    sizes = {L: ws(1 << 16, L, 32, 8, 128, 8)[1] for L in (1000, 1100, 1200, 1300)}
+    assert min(sizes.values()) <= SCRATCH_BYTES < max(sizes.values())
+    for L, b in sizes.items():
+        if b > SCRATCH_BYTES:
+            assert noalloc(mocap_lib, P=1 << 16, L=L, n_table=((1 << 16) + L) // 256 + 1, splits=8) == WORKSPACE
+
+
+def test_noalloc_zero_length_chunk_is_a_noop(mocap_lib):
+    assert noalloc(mocap_lib, L=0, q=0, o=0, lse=0) == 0
