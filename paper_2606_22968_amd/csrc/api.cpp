@@ -59,12 +59,13 @@ mocap_status device_cu_count(int* out) {
   return MOCAP_OK;
 }
 
-// Query heads per workgroup: the largest of 4, 2, 1 dividing the GQA group.
-int heads_per_wg(int group) { return group % 4 == 0 ? 4 : (group % 2 == 0 ? 2 : 1); }
+// Query heads per unit (four waves): 2 when the GQA group is even, else 1.
+int heads_per_unit(int group) { return group % 2 == 0 ? 2 : 1; }
 
 struct Plan {
-  int hp;
+  int hu;
   int row_groups;
+  int pairs;
   int base_wgs;      // workgroups of one KV range
   int64_t prefix_tiles;
   int n_ranges;
@@ -82,9 +83,11 @@ size_t workspace_for(int n_ranges, int64_t chunk_len, int h_q, int head_dim) {
 }
 
 // Time model of one launch, used to choose the number of KV ranges.
-//   * A workgroup costs kTileUs per 64-key tile it visits (scaled by
-//     head_dim / 128) plus kGroupUs of fixed work; one workgroup per compute
-//     unit at a time (the attention kernel's LDS ring fills a CU).
+//   * A workgroup costs kTileUs per 64-key tile that both of its units
+//     compute and kLoneTile times that for a tile only its longer unit
+//     computes (one wave per SIMD), scaled by head_dim / 128, plus kGroupUs
+//     of fixed work; one workgroup per compute unit at a time (the attention
+//     kernel's LDS ring fills a CU).
 //   * The launch time is the makespan of longest-first list scheduling of
 //     all workgroups onto the compute units (the kernel orders its work items
 //     longest first), plus, when split, the partial-result traffic (written
@@ -95,28 +98,31 @@ constexpr double kTileUs = 2.0;
 constexpr double kGroupUs = 4.0;
 constexpr double kMergeBytesPerUs = 3.0e6;
 constexpr double kLaunchUs = 4.0;
+constexpr double kLoneTile = 0.65;
 
 double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int head_dim, int head_blocks_total,
-                          int row_groups, int rows_per_wg, int64_t prefix_tiles, int n_ranges, int slots) {
+                          int row_groups, int rows_per_unit, int64_t prefix_tiles, int n_ranges, int slots) {
   std::vector<double> cost;
-  cost.reserve((size_t)head_blocks_total * row_groups * n_ranges);
+  const int pairs = (row_groups + 1) / 2;
+  cost.reserve((size_t)head_blocks_total * pairs * n_ranges);
   const double tile_us = kTileUs * head_dim / 128.0;
-  for (int rg = 0; rg < row_groups; ++rg) {
-    const int64_t row_end = std::min<int64_t>(chunk_len, (int64_t)(rg + 1) * rows_per_wg);
-    if (n_ranges == 1) {
-      const int64_t tiles = (prefix_len + row_end + kTileKeys - 1) / kTileKeys;
-      for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back(tiles * tile_us + kGroupUs);
-    } else {
-      const int64_t t0 = prefix_len / kTileKeys;
-      const int64_t t1 = (prefix_len + row_end + kTileKeys - 1) / kTileKeys;
-      for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back((t1 - t0) * tile_us + kGroupUs);
-    }
+  // Tiles the unit of row group rg visits in the range that holds the chunk's keys.
+  auto unit_tiles = [&](int rg) -> int64_t {
+    const int64_t row_end = std::min<int64_t>(chunk_len, (int64_t)(rg + 1) * rows_per_unit);
+    const int64_t t0 = n_ranges == 1 ? 0 : prefix_len / kTileKeys;
+    return (prefix_len + row_end + kTileKeys - 1) / kTileKeys - t0;
+  };
+  for (int q = 0; q < pairs; ++q) {
+    const int64_t a = unit_tiles(q);
+    const int64_t b = q == row_groups - 1 - q ? 0 : unit_tiles(row_groups - 1 - q);
+    const double us = (double)std::min(a, b) * tile_us + (double)(std::max(a, b) - std::min(a, b)) * kLoneTile * tile_us;
+    for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back(us + kGroupUs);
   }
   if (n_ranges > 1) {
     const int parts = n_ranges - 1;
     for (int r = 0; r < parts; ++r) {
       const int64_t tiles = prefix_tiles * (r + 1) / parts - prefix_tiles * r / parts;
-      for (int i = 0; i < head_blocks_total * row_groups; ++i) cost.push_back(tiles * tile_us + kGroupUs);
+      for (int i = 0; i < head_blocks_total * pairs; ++i) cost.push_back(tiles * tile_us + kGroupUs);
     }
   }
   std::sort(cost.begin(), cost.end(), std::greater<double>());
@@ -161,7 +167,7 @@ int g_plan_count = 0, g_plan_next = 0;
 // ws_cap bytes, or no split at all, the plan with the smallest modelled
 // launch time.
 int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int head_dim, int head_blocks_total,
-                  int row_groups, int rows_per_wg, int64_t prefix_tiles, int requested, int slots,
+                  int row_groups, int rows_per_unit, int64_t prefix_tiles, int requested, int slots,
                   size_t ws_cap) {
   if (prefix_tiles <= 0) return 1;
   if (requested >= 1) {
@@ -177,12 +183,12 @@ int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int 
   }
   int best = 1;
   double best_us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
-                                      rows_per_wg, prefix_tiles, 1, slots);
+                                      rows_per_unit, prefix_tiles, 1, slots);
   const int64_t max_parts = std::min<int64_t>(16, prefix_tiles / 4);
   for (int64_t parts = 1; parts <= max_parts; parts *= 2) {
     if (workspace_for((int)parts + 1, chunk_len, h_q, head_dim) > ws_cap) break;
     const double us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
-                                         rows_per_wg, prefix_tiles, (int)parts + 1, slots);
+                                         rows_per_unit, prefix_tiles, (int)parts + 1, slots);
     if (us < best_us * 0.98) {  // a split must pay for itself clearly
       best_us = us;
       best = (int)parts + 1;
@@ -199,10 +205,11 @@ int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int 
 mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
                        int32_t head_dim, int32_t num_splits, Plan* plan, size_t ws_cap = SIZE_MAX) {
   const int group = h_q / h_kv;
-  plan->hp = heads_per_wg(group);
-  const int rows_per_wg = kAttnWaveRows * (kAttnWaves / plan->hp);
-  plan->row_groups = (int)((chunk_len + rows_per_wg - 1) / rows_per_wg);
-  const int64_t base = (int64_t)(h_q / plan->hp) * plan->row_groups;
+  plan->hu = heads_per_unit(group);
+  const int rows_per_unit = kAttnWaveRows * (kAttnWaves / 2 / plan->hu);
+  plan->row_groups = (int)((chunk_len + rows_per_unit - 1) / rows_per_unit);
+  plan->pairs = (plan->row_groups + 1) / 2;
+  const int64_t base = (int64_t)(h_q / plan->hu) * plan->pairs;
   if (base > (int64_t)1 << 24) return MOCAP_ERR_UNSUPPORTED;
   plan->base_wgs = (int)base;
   plan->prefix_tiles = (prefix_len + kTileKeys - 1) / kTileKeys;
@@ -211,8 +218,8 @@ mocap_status make_plan(int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32
     const mocap_status st = device_cu_count(&cus);
     if (st != MOCAP_OK) return st;
   }
-  plan->n_ranges = choose_ranges(prefix_len, chunk_len, h_q, h_kv, head_dim, h_q / plan->hp, plan->row_groups,
-                                 rows_per_wg, plan->prefix_tiles, num_splits, cus, ws_cap);
+  plan->n_ranges = choose_ranges(prefix_len, chunk_len, h_q, h_kv, head_dim, h_q / plan->hu, plan->row_groups,
+                                 rows_per_unit, plan->prefix_tiles, num_splits, cus, ws_cap);
   plan->ws_bytes = workspace_for(plan->n_ranges, chunk_len, h_q, head_dim);
   return MOCAP_OK;
 }
@@ -291,8 +298,9 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   p.h_q = h_q;
   p.h_kv = h_kv;
   p.group = h_q / h_kv;
-  p.heads_per_wg = plan.hp;
+  p.heads_per_unit = plan.hu;
   p.row_groups = plan.row_groups;
+  p.pairs = plan.pairs;
   p.block_size = kv->block_size;
   block_divider((uint32_t)kv->block_size, &p.block_magic, &p.block_shift);
   p.n_ranges = plan.n_ranges;

@@ -10,6 +10,12 @@
 //     as the B operand of the score product.  All wavefronts of a workgroup
 //     share one KV head (GQA packing), so each K/V tile staged in LDS serves
 //     every query head of the group.
+//   * Causal balance: the workgroup's two units of four waves take row
+//     groups r and R-1-r of the same query heads, so every workgroup carries
+//     about the same number of (row, key) pairs.  Each wave follows its own
+//     key range: it stops computing after the last tile its rows see (the
+//     other unit's wave on its SIMD then has the SIMD alone) and treats the
+//     tiles all its rows see in full as unmasked.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
 //     (buffer_load_dwordx4 ... lds, no staging registers) into a 4-stage ring
 //     (128 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
@@ -78,33 +84,38 @@ __device__ __forceinline__ int key_row_order(int m) {
 
 struct WorkItem {
   int kv_head;
-  int head0;      // first query head of the workgroup
-  int row_group;  // index of the workgroup's block of rows
-  int range;      // KV range index
+  int head0;        // first query head of both units
+  int row_group_a;  // row group of waves 0-3
+  int row_group_b;  // row group of waves 4-7 (-1: none)
+  int range;        // KV range index
 };
 
 // Workgroup ids are handed to the 8 XCDs round robin.  Renumber them so each
 // XCD receives one contiguous run of logical items: consecutive items share a
 // KV head, so the tiles they stream stay in that XCD's L2.  Within a KV head
-// the logical order is range, then row group from the last (longest) one
-// down, then the head blocks of the group.
+// the logical order is range, then row-group pair (pair q holds row groups q
+// and R-1-q; the middle group of an odd R is alone), then the head blocks of
+// the group.
 __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) {
   const int n = p.total_wgs;
   const int xcd = hw_id & 7, slot = hw_id >> 3;
   const int per = n >> 3, rem = n & 7;
   const int logical = xcd * per + min(xcd, rem) + slot;
 
-  const int head_blocks = p.group / p.heads_per_wg;
-  const int per_range = head_blocks * p.row_groups;
+  const int head_blocks = p.group / p.heads_per_unit;
+  const int per_range = head_blocks * p.pairs;
   const int per_kv = per_range * p.n_ranges;
   WorkItem w;
   w.kv_head = logical / per_kv;
   int r = logical - w.kv_head * per_kv;
   w.range = r / per_range;
   r -= w.range * per_range;
-  w.row_group = p.row_groups - 1 - r / head_blocks;
-  const int hb = r - (r / head_blocks) * head_blocks;
-  w.head0 = w.kv_head * p.group + hb * p.heads_per_wg;
+  const int pair = r / head_blocks;
+  const int hb = r - pair * head_blocks;
+  w.row_group_a = pair;
+  w.row_group_b = p.row_groups - 1 - pair;
+  if (w.row_group_b == pair) w.row_group_b = -1;
+  w.head0 = w.kv_head * p.group + hb * p.heads_per_unit;
   return w;
 }
 
@@ -198,12 +209,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const WorkItem item = decode_item(p, blockIdx.x);
   const int P = p.prefix_len;
   const int L = p.chunk_len;
-  const int hp = p.heads_per_wg;
-  const int blocks_per_wg = kAttnWaves / hp;
-  const int head = item.head0 + (wave % hp);
-  const int wg_row0 = item.row_group * blocks_per_wg * kAttnWaveRows;
-  const int row0 = wg_row0 + (wave / hp) * kAttnWaveRows;
-  const int wg_row_end = min(L, (item.row_group + 1) * blocks_per_wg * kAttnWaveRows);
+  // Waves 0-3 form unit A, waves 4-7 unit B (one wave of each per SIMD).
+  const int hu = p.heads_per_unit;
+  const int unit_rows = (kAttnWaves / 2 / hu) * kAttnWaveRows;
+  const int uw = wave & 3;
+  const int head = item.head0 + (uw % hu);
+  const int my_rg = (wave >> 2) == 0 ? item.row_group_a : item.row_group_b;
+  const int row0_unclamped = my_rg * unit_rows + (uw / hu) * kAttnWaveRows;
+  const bool wave_on = my_rg >= 0 && row0_unclamped < L;  // a wave whose rows all lie past L has nothing to do
+  const int row0 = max(my_rg, 0) * unit_rows + (uw / hu) * kAttnWaveRows;
+  const int wg_row0 = item.row_group_a * unit_rows;
+  const int wg_row_end = min(L, (max(item.row_group_a, item.row_group_b) + 1) * unit_rows);
 
   int lo, hi;
   if (p.n_ranges == 1) {
@@ -231,6 +247,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     if (i < n_fast + n_head) return tile_begin;
     return fast_end + (i - n_fast - n_head);
   };
+  // This wave's share of the sequence: the first n_w positions (the tiles
+  // its rows see; tiles past them come last in the order above), and, among
+  // them, the tiles every one of its rows sees in full (unmasked).
+  const int w_tile_end = (min(hi, P + row0 + kAttnWaveRows) + kTileKeys - 1) / kTileKeys;
+  const int n_w = wave_on ? n_tiles - max(0, tile_end - w_tile_end) : 0;
+  const int w_full_end = min(hi, P + row0 + 1);
+  auto masked_at = [&](int i) __attribute__((always_inline)) -> bool {
+    const int t = seq_tile(i);
+    return t * kTileKeys < lo || (t + 1) * kTileKeys > w_full_end;
+  };
 
   // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T).
   bf16x8 qf[KS];
@@ -250,15 +276,21 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const int64_t head_stride = (int64_t)D * p.block_size;
   const int my_group = wave >> 2;
   const int gwave = wave & 3;  // wave within its group of four
-  int k_src[LOADS], v_src[LOADS];
-#pragma unroll
-  for (int j = 0; j < LOADS; ++j) {
-    const int chunk = (j * 4 + gwave) * 64 + lane;
+  // Copy j of a tile moves 16-byte chunk (j * 4 + gwave) * 64 + lane.  The
+  // swizzled column of a chunk does not depend on j (j adds whole rows: 16 K
+  // rows or 32 V dim rows), so one per-lane offset serves every copy and j
+  // moves the scalar offset.
+  int k_src, v_src;
+  {
+    const int chunk = gwave * 64 + lane;
     const int kr = chunk / K_ROW_CHUNKS, kc = (chunk % K_ROW_CHUNKS) ^ k_swizzle<D>(kr);
-    k_src[j] = kr * D + kc * 8;
+    k_src = (kr * D + kc * 8) * 2;
     const int vr = chunk / V_ROW_CHUNKS, vc = (chunk % V_ROW_CHUNKS) ^ v_swizzle(vr);
-    v_src[j] = vr * p.block_size + vc * 8;
+    v_src = (vr * p.block_size + vc * 8) * 2;
   }
+  constexpr int K_ROWS_PER_COPY = kAttnThreads / 2 / K_ROW_CHUNKS;
+  constexpr int V_ROWS_PER_COPY = kAttnThreads / 2 / V_ROW_CHUNKS;
+  static_assert(K_ROWS_PER_COPY % 16 == 0 && V_ROWS_PER_COPY % 16 == 0, "copy stride keeps the swizzle");
   auto issue_seq = [&](int i) __attribute__((always_inline)) {
     if ((i & 1) != my_group) return;
     const int t = seq_tile(i);
@@ -281,8 +313,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int dst = (j * 4 + gwave) * 64 * 8;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(kl + dst), 16, k_src[j] * 2, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(vl + dst), 16, v_src[j] * 2, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(kl + dst), 16, k_src, j * K_ROWS_PER_COPY * D * 2,
+                                               0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(vl + dst), 16, v_src,
+                                               j * V_ROWS_PER_COPY * p.block_size * 2, 0, 0);
     }
   };
   // The group that copied tile i waits for its copies (the only ones it has in
@@ -507,19 +541,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     publish_seq(k);
     if (k + 2 < n_tiles) issue_seq(k + 2);
   };
-  // Tile i: scores, then the previous tile's P*V with this tile's
-  // probabilities woven in, so one wave keeps both the matrix and the vector
-  // units busy; the probabilities alternate between two buffers.  Tile 0 has
-  // no predecessor.
-  auto first_tile = [&](bool masked) __attribute__((always_inline)) {
-    barrier_k(0);
-    scores(0, masked);
-    probs(0, -m_run);
-    settle(0);
-  };
-  auto next_tile = [&](int i, int b, bool masked) __attribute__((always_inline)) {
+  // Position i of the sequence (probabilities into buffer b): scores, then
+  // the previous tile's P*V with this tile's probabilities woven in, so one
+  // wave keeps both the matrix and the vector units busy.
+  auto step = [&](int i, int b) __attribute__((always_inline)) {
     barrier_k(i);
-    scores(i, masked);
+    scores(i, masked_at(i));
     pv_probs(i - 1, b ^ 1, b, -m_run);
     settle(b);
   };
@@ -531,22 +558,29 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     asm volatile("" : "+s"(lo), "+s"(hi), "+v"(k_row_lo), "+v"(v_row_sw));
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
-    if (n_fast > 0) {
-      first_tile(false);
-    } else {
-      first_tile(true);
+    barrier_k(0);
+    if (n_w > 0) {
+      scores(0, masked_at(0));
+      probs(0, -m_run);
+      settle(0);
     }
-    for (int i = 1; i < n_tiles; i += 2) {
-      next_tile(i, 1, i >= n_fast);
-      if (i + 1 < n_tiles) next_tile(i + 1, 0, i + 1 >= n_fast);
+    // The wave computes positions [0, n_w), finishes the P*V of its last
+    // tile, then only copies tiles and meets the remaining barriers (every
+    // wave meets barrier k once, in order, for every k < n_tiles).
+    for (int i = 1; i < n_w; i += 2) {
+      step(i, 1);
+      if (i + 1 < n_w) step(i + 1, 0);
     }
-    if ((n_tiles - 1) & 1) {  // the last tile's probabilities are in buffer 1
+    if (n_w > 0) {
+      if ((n_w - 1) & 1) {  // the last tile's probabilities are in buffer 1
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
+          for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
+      }
+      pv(n_w - 1, 0);
     }
-    pv(n_tiles - 1, 0);
+    for (int i = max(n_w, 1); i < n_tiles; ++i) barrier_k(i);
     lds_barrier();  // every wave is done with the tiles
     if (tid == 0) *rerun_flag = 0;
     lds_barrier();
@@ -568,7 +602,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const float l_tot = lane_pair_sum(l_run);
   const float f_tot = lane_pair_sum(f_run);
   const int row = row0 + l32;
-  if (row < L) {
+  if (wave_on && row < L) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float row_lse = f_tot > 0.f ? (m_run + log2f(f_tot)) * kLn2 : -INFINITY;
     if (!split) {
