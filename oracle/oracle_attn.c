@@ -70,12 +70,18 @@ int oracle_chunk_attn(const void* q, const void* k, const void* v, int is_bf16,
   {
     double* s = (double*)malloc(sizeof(double) * (size_t)(max_keys > 0 ? max_keys : 1));
     double* acc = (double*)malloc(sizeof(double) * (size_t)d);
-    if (!s || !acc) {
+    const int have_buffers = s != NULL && acc != NULL;
+    if (!have_buffers) {
 #pragma omp atomic write
       bad_alloc = 1;
-    } else {
+    }
+    /* Every thread of the team reaches the work-sharing loop (OpenMP
+       requires it); a thread without buffers takes no task, and the call
+       then reports -2. */
+    {
 #pragma omp for schedule(dynamic, 1)
       for (int64_t task = 0; task < n_rows * h_q; ++task) {
+        if (!have_buffers) continue;
         const int64_t r = task / h_q;
         const int h = (int)(task % h_q);
         const int64_t i = rows[r];

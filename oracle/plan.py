@@ -59,11 +59,6 @@ def balance_cost(chunk_len, prefix_len):
     return chunk_len * (prefix_len + chunk_len / 2.0)
 
 
-def eq1_cost(chunk_len, prefix_len):
-    """Eq. (1) attention proxy of the paper: c_i (p_i + c_i)."""
-    return chunk_len * (prefix_len + chunk_len)
-
-
 def causal_flops(lengths, h_q, head_dim):
     """Algorithmic FLOPs of QK^T and PV over visible pairs: 4 d Hq pairs."""
     pairs = sum(visible_pairs(n, p) for n, p in zip(lengths, prefixes(lengths)))
