@@ -12,11 +12,21 @@ Prints ONE JSON line:
   roofline   the attention kernel's algorithmic FLOPs per launch over its
              average launch duration (HIP events on the launch stream), against
              the bf16 dense MFMA peak
-  cpu_baseline  the fp64 oracle on this host's cores over a bounded sample
-             of the same workload (every chunk x every head x 64 rows, about ten
-             seconds on 16 cores)
+  clock      the attention kernel's average graphics clock from the committed
+             rocprofv3 counter profile of this workload (GRBM_GUI_ACTIVE cycles
+             per XCD over each dispatch's duration), when that profile was
+             taken on the current kernel source; and the kernel's fraction of
+             the bf16 peak at that clock (256 CUs x 4096 FLOP per clock)
+  cpu_baseline  the fp64 oracle on this host's cores: the 1024-token d64
+             workload in full, then the parity row sample of the benchmark
+             workload (every chunk x every head x 8 rows) and its last chunk
+             in full; the measured fp64 rate, and the full workload's oracle
+             time projected from it (about a minute of CPU work)
 
 Usage: python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+       python bench.py --summarize-trace KERNEL_TRACE_CSV [--steps K] [--workload NAME]
+           (summary of the attention launches of the timed steps in a
+            rocprofv3 --kernel-trace run of this script)
 """
 import argparse
 import json
@@ -29,6 +39,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16: 256 CUs x 4096 FLOP/clk x 2.4 GHz
+FLOP_PER_CLOCK = 256 * 4096      # dense bf16 MFMA FLOP per clock over the whole chip
 METRIC = "chunked-prefill attention causal TFLOP/s & % bf16 MFMA peak; per-chunk latency"
 
 
@@ -43,20 +54,23 @@ def parse():
                     help="hold the KV of the first fraction of the sequence (whole blocks) in a second store, "
                          "as a debtor stage's remote portion, and read it with the two-store call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=64, help="oracle rows per (chunk, head)")
+    ap.add_argument("--cpu-rows", type=int, default=8, help="oracle sample rows per (chunk, head)")
+    ap.add_argument("--summarize-trace", default=None,
+                    help="print a summary of a rocprofv3 kernel trace of this script and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel for scaling a profiler's FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
-def recorded_traffic(workload):
-    """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE, calibrated against a device copy), or
-    None when there is none for this workload or the kernel source changed
+def recorded_counters(workload):
+    """Counter figures of the attention kernel from the committed rocprofv3
+    summary of this workload (HBM bytes per launch from FETCH_SIZE and
+    WRITE_SIZE scaled by a device-copy calibration; average clock from
+    GRBM_GUI_ACTIVE), or None when there is none or the kernel source changed
     since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"chunk_attn_{workload.replace('_uniform', '')}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"chunk_attn_{workload}_counters.json")
     src = os.path.join(ROOT, "paper_2606_22968_amd", "csrc", "chunk_attn.hip")
     if not os.path.exists(path):
         return None
@@ -65,7 +79,7 @@ def recorded_traffic(workload):
     with open(src, "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != rec.get("kernel_source_sha256"):
             return None
-    return rec["avg_traffic_bytes_per_launch"]
+    return rec
 
 
 def causal_pairs(lengths):
@@ -77,32 +91,88 @@ def causal_pairs(lengths):
 
 
 def cpu_baseline(w, q, k, v, lengths, rows_per_chunk):
-    """Time the fp64 oracle on a bounded sample of the workload."""
+    """Time the fp64 oracle: the small workload in full, then a row sample of
+    the benchmark workload and its last chunk in full."""
     import oracle
     from paper_2606_22968_amd import synth
 
-    qb, kb, vb = synth.bf16_bits(q), synth.bf16_bits(k), synth.bf16_bits(v)
-    flops, p = 0, 0
+    def run_chunks(wl, qb, kb, vb, plan, rows_of):
+        flops, p = 0, 0
+        for c, n in enumerate(plan):
+            rows = rows_of(c, n)
+            oracle.chunk_attn(qb[p:p + n], kb[:p + n], vb[:p + n], p, wl.scale, rows=rows)
+            rows = range(n) if rows is None else rows
+            flops += sum(4 * wl.head_dim * wl.h_q * (p + r + 1) for r in rows)
+            p += n
+        return flops
+
+    w0 = synth.WORKLOADS["small_d64"]
+    q0, k0, v0 = synth.make_qkv(w0.seed, w0.seq_len, w0.h_q, w0.h_kv, w0.head_dim)
+    plan0 = [w0.seq_len // w0.num_chunks] * w0.num_chunks
     t0 = time.perf_counter()
-    for c, n in enumerate(lengths):
-        rows = synth.sample_rows(n, 1000 * w.seed + c, n_random=max(rows_per_chunk - 5, 0))
-        oracle.chunk_attn(qb[p:p + n], kb, vb, p, w.scale, rows=rows)
-        flops += sum(4 * w.head_dim * w.h_q * (p + r + 1) for r in rows)
-        p += n
-    dt = time.perf_counter() - t0
+    f0 = run_chunks(w0, synth.bf16_bits(q0), synth.bf16_bits(k0), synth.bf16_bits(v0), plan0, lambda c, n: None)
+    small_s = time.perf_counter() - t0
+
+    qb, kb, vb = synth.bf16_bits(q), synth.bf16_bits(k), synth.bf16_bits(v)
+    t0 = time.perf_counter()
+    f_rows = run_chunks(w, qb, kb, vb, lengths, lambda c, n: synth.sample_rows(
+        n, 1000 * w.seed + c, n_random=max(rows_per_chunk - 5, 0)))
+    rows_s = time.perf_counter() - t0
+    p_last, n_last = sum(lengths[:-1]), lengths[-1]
+    t0 = time.perf_counter()
+    oracle.chunk_attn(qb[p_last:], kb, vb, p_last, w.scale)
+    last_s = time.perf_counter() - t0
+    f_last = 4 * w.head_dim * w.h_q * (n_last * p_last + n_last * (n_last + 1) // 2)
+    rate = (f_rows + f_last) / (rows_s + last_s)
+    full = 4 * w.head_dim * w.h_q * causal_pairs(lengths)
     return {
-        "value": flops / dt / 1e12,
+        "value": rate / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.max_threads(),
         "kind": "oracle",
-        "sample": (f"{w.name}: every chunk x all {w.h_q} heads x {rows_per_chunk} rows "
-                   f"(edges, middle, seeded random); {flops / 1e9:.1f} GFLOP fp64 in {dt:.1f} s; "
-                   f"host has {os.cpu_count()} logical CPUs"),
+        "sample": (f"{w0.name} in full ({f0 / 1e9:.2f} GFLOP, {small_s:.2f} s); {w.name}: every chunk x "
+                   f"{w.h_q} heads x {rows_per_chunk} rows ({f_rows / 1e9:.0f} GFLOP, {rows_s:.1f} s) and the "
+                   f"last chunk in full ({f_last / 1e12:.3f} TFLOP, {last_s:.1f} s); fp64, "
+                   f"{os.cpu_count()} logical CPUs"),
+        "gflops_fp64": round(rate / 1e9, 2),
+        "small_d64_full_s": round(small_s, 3),
+        "last_chunk_full_s": round(last_s, 2),
+        "projected_full_s": round(full / rate, 1),
+        "projected": True,
     }
+
+
+def summarize_trace(path, workload, steps):
+    """Attention launches of the last `steps` steps of a rocprofv3 kernel trace
+    (CSV) of this script: the timed passes, without the warm-up ones."""
+    import csv
+    from paper_2606_22968_amd import binding, synth
+    w = synth.WORKLOADS[workload]
+    lengths = binding.mocap_chunk_plan(w.seq_len, w.num_chunks, w.align, balanced=(w.chunking == "balanced"))
+    rows = list(csv.DictReader(open(path)))
+    attn = [r for r in rows if "chunk_attn_kernel" in r["Kernel_Name"]]
+    n = steps * len(lengths)
+    if len(attn) < n:
+        raise SystemExit(f"{path}: {len(attn)} attention launches, fewer than {steps} steps x {len(lengths)}")
+    timed = attn[-n:]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in timed]  # us
+    per_chunk = [statistics.median(dur[s * len(lengths) + c] for s in range(steps)) for c in range(len(lengths))]
+    flops = 4 * w.head_dim * w.h_q * causal_pairs(lengths)
+    step_us = sum(dur) / steps
+    achieved = flops / (step_us * 1e-6) / 1e12
+    names = sorted({r["Kernel_Name"] for r in timed})
+    print(f"kernel(s): {', '.join(names)}")
+    print(f"timed steps: {steps} x {len(lengths)} launches (the last {n} attention launches of the trace)")
+    print(f"average launch: {statistics.mean(dur):.1f} us; attention per step: {step_us / 1e3:.4f} ms")
+    print(f"achieved: {achieved:.1f} TFLOP/s = {achieved / MFMA_BF16_PEAK_TFLOPS:.4f} of {MFMA_BF16_PEAK_TFLOPS}")
+    print("per-chunk median us: " + ", ".join(f"{x:.1f}" for x in per_chunk))
 
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.workload, args.steps)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(--gpus N with N > 1 is not supported).", file=sys.stderr)
@@ -150,6 +220,7 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
+
     ms_per_step = elapsed * 1e3 / args.steps
     pairs = causal_pairs(lengths)
     flops = 4 * w.head_dim * w.h_q * pairs
@@ -165,6 +236,13 @@ def main():
     # over the average launch duration.
     achieved = flops / (attn_total_ms * 1e-3) / 1e12
     split_chunks = sum(1 for r in runner.splits if r > 1)
+    counters = recorded_counters(w.name)
+    clk = None
+    if counters and counters.get("avg_clock_ghz"):
+        peak_at_clock = FLOP_PER_CLOCK * counters["avg_clock_ghz"] * 1e9 / 1e12
+        clk = {"ghz": counters["avg_clock_ghz"], "peak_tflops_at_clock": round(peak_at_clock, 1),
+               "frac_at_clock": round(achieved / peak_at_clock, 4),
+               "source": f"profiles/chunk_attn_{w.name}_counters.json (rocprofv3 GRBM_GUI_ACTIVE)"}
 
     result = {
         "metric": METRIC,
@@ -190,6 +268,7 @@ def main():
             "parallelism": "single GPU",
         },
         "pct_of_bf16_peak": round(100.0 * value / MFMA_BF16_PEAK_TFLOPS, 2),
+        "clock": clk,
         "per_chunk_us": [round(x, 1) for x in chunk_us],
         "per_chunk_max_over_min": round(max(chunk_us) / min(chunk_us), 2),
         "attention_ms_per_step": round(attn_total_ms, 4),
@@ -202,7 +281,7 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": recorded_traffic(w.name),
+            "traffic": counters.get("avg_traffic_bytes_per_launch") if counters else None,
             "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE)",
             "launches_per_step": n_chunks,
             "includes_merge_launches": split_chunks > 0,
