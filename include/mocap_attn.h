@@ -302,9 +302,9 @@ mocap_status mocap_lbcp_plan_table(int64_t seq_len, int32_t num_chunks, int32_t 
  * (the top 53 bits) the acceptance.
  *
  * The latency of a partition is its single-request prefill latency under
- * the same table: sum of chunk costs + (num_stages - 1) * largest chunk cost.
- * The paper's EvaluatePrefill / EvaluateE2E also model the feasible batch
- * size and end-to-end queueing, which are outside this library.
+ * the same table: sum of chunk costs + (num_stages - 1) * largest chunk cost
+ * (a single-request refinement; mocap_lbcp_refine_e2e adds the paper's
+ * batch, memory and end-to-end terms).
  *
  *   chunk_cost     as in mocap_lbcp_plan_table
  *   temp0 > 0, temp_min > 0, 0 < alpha < 1, rounds >= 1
@@ -317,6 +317,79 @@ mocap_status mocap_lbcp_plan_table(int64_t seq_len, int32_t num_chunks, int32_t 
 mocap_status mocap_lbcp_refine(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
                                const double* chunk_cost, double temp0, double temp_min, double alpha,
                                int32_t rounds, uint64_t seed, int32_t* lengths_inout, double* latency_out);
+
+/*
+ * The serving model of mocap_lbcp_evaluate and mocap_lbcp_refine_e2e: the
+ * batch size, memory and end-to-end terms of Section 4.2's second stage
+ * (EvaluatePrefill and EvaluateE2E of Alg. 1), which the paper names without
+ * defining.  The readings this library takes:
+ *   - N identical pipeline stages run the chunk operations of `requests`
+ *     requests waiting at time 0, served in order in batches of B (the last
+ *     one smaller); consecutive batches follow each other through the
+ *     pipeline.  A chunk of a batch of n requests takes t + (n - 1) *
+ *     max(t - fixed_cost, 0) on every stage, t being its table entry (the
+ *     latency for one request) and fixed_cost the part of it a batch does
+ *     not multiply.
+ *   - A stage holds the KV of a batch's chunks from the start of each chunk
+ *     on that stage until the batch leaves the last stage (Section 3.1:
+ *     earlier stages hold theirs longer).  One request token occupies
+ *     kv_bytes_per_token on a stage; each stage holds stage_capacity bytes of
+ *     KV.  pairing = 0: every stage must fit its own capacity at all times;
+ *     pairing = 1 (Section 4.1's memory-balanced reallocation with fixed
+ *     cross-half pairing, N even): stage i and stage i + N/2 pool their
+ *     capacities (a debtor spills to its partner).
+ *   - EvaluatePrefill gives B', the largest batch in [1, min(max_batch,
+ *     requests)] whose schedule fits (0 if none), and T'_pre, the prefill
+ *     latency of one batch of B' (sum of its chunk times + (N - 1) times the
+ *     largest); EvaluateE2E gives T', the completion time of the last of
+ *     the requests served in batches of B' (the workload's end-to-end
+ *     latency; requests / T' is its throughput; +infinity when B' = 0).
+ */
+typedef struct {
+  double fixed_cost;          /* >= 0, in the units of the cost table        */
+  double kv_bytes_per_token;  /* > 0                                          */
+  double stage_capacity;      /* > 0, bytes of KV one stage holds             */
+  int32_t pairing;            /* 0 or 1                                       */
+  int32_t max_batch;          /* 1 .. 4096                                    */
+  int32_t requests;           /* 1 .. 4096                                    */
+} mocap_lbcp_serving;
+
+/*
+ * mocap_lbcp_evaluate -- EvaluatePrefill and EvaluateE2E of one partition
+ * under the serving model above (host only).
+ *
+ *   chunk_cost  as in mocap_lbcp_plan_table
+ *   serving     the serving model
+ *   lengths     host int32 [num_chunks], a partition of seq_len into positive
+ *               multiples of align
+ *   batch_out, t_pre_out, t_e2e_out   (each may be NULL) B', T'_pre, T'
+ * Errors: INVALID_ARG for malformed sizes, table, serving model (pairing with
+ * odd num_stages included) or partition; UNSUPPORTED as in mocap_lbcp_plan.
+ */
+mocap_status mocap_lbcp_evaluate(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                                 const double* chunk_cost, const mocap_lbcp_serving* serving,
+                                 const int32_t* lengths, int32_t* batch_out, double* t_pre_out,
+                                 double* t_e2e_out);
+
+/*
+ * mocap_lbcp_refine_e2e -- second stage of latency-balanced chunk
+ * partitioning (Section 4.2, Alg. 1's simulated annealing) under the serving
+ * model: every candidate partition is scored by (B', T'_pre) =
+ * EvaluatePrefill, T' = EvaluateE2E, and T' is minimised.  Perturbation,
+ * acceptance, cooling and random draws are those of mocap_lbcp_refine (a
+ * candidate with T' = +infinity is never accepted over a finite one).
+ *
+ *   lengths_inout  in: the start partition (typically the dynamic program's);
+ *                  out: the best one found
+ *   batch_out, t_pre_out, t_e2e_out   (each may be NULL) its B', T'_pre, T'
+ * Other arguments as in mocap_lbcp_refine and mocap_lbcp_evaluate.
+ * Errors: as mocap_lbcp_evaluate, plus INVALID_ARG for a malformed schedule.
+ */
+mocap_status mocap_lbcp_refine_e2e(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
+                                   const double* chunk_cost, const mocap_lbcp_serving* serving, double temp0,
+                                   double temp_min, double alpha, int32_t rounds, uint64_t seed,
+                                   int32_t* lengths_inout, int32_t* batch_out, double* t_pre_out,
+                                   double* t_e2e_out);
 
 /*
  * Bytes of the library's static device scratch used by

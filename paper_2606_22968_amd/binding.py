@@ -36,8 +36,21 @@ EXPORTED = (
     "mocap_lbcp_plan",
     "mocap_lbcp_plan_table",
     "mocap_lbcp_refine",
+    "mocap_lbcp_evaluate",
+    "mocap_lbcp_refine_e2e",
     "mocap_status_string",
 )
+
+
+class mocap_lbcp_serving(ctypes.Structure):
+    _fields_ = [
+        ("fixed_cost", ctypes.c_double),
+        ("kv_bytes_per_token", ctypes.c_double),
+        ("stage_capacity", ctypes.c_double),
+        ("pairing", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32),
+        ("requests", ctypes.c_int32),
+    ]
 
 
 class MocapError(RuntimeError):
@@ -117,6 +130,17 @@ def load_library():
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
         ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32, ctypes.c_uint64,
         ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)]
+    lib.mocap_lbcp_evaluate.restype = st
+    lib.mocap_lbcp_evaluate.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+        ctypes.POINTER(mocap_lbcp_serving), ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    lib.mocap_lbcp_refine_e2e.restype = st
+    lib.mocap_lbcp_refine_e2e.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+        ctypes.POINTER(mocap_lbcp_serving), ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32,
+        ctypes.c_uint64, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     lib.mocap_chunk_plan.restype = st
     lib.mocap_chunk_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -337,3 +361,39 @@ def mocap_lbcp_refine(seq_len: int, num_chunks: int, num_stages: int, align: int
                                             int(seed) & 0xFFFFFFFFFFFFFFFF, io, ctypes.byref(lat)),
            "mocap_lbcp_refine")
     return list(io), lat.value
+
+
+def _serving(fixed_cost: float, kv_bytes_per_token: float, stage_capacity: float, pairing: bool,
+             max_batch: int, requests: int) -> mocap_lbcp_serving:
+    return mocap_lbcp_serving(float(fixed_cost), float(kv_bytes_per_token), float(stage_capacity),
+                              1 if pairing else 0, int(max_batch), int(requests))
+
+
+def mocap_lbcp_evaluate(seq_len: int, num_chunks: int, num_stages: int, align: int, chunk_cost,
+                        lengths: Sequence[int], fixed_cost: float, kv_bytes_per_token: float,
+                        stage_capacity: float, pairing: bool, max_batch: int, requests: int):
+    """Returns (B', T'_pre, T') of a partition under the serving model."""
+    arr, ptr = _cost_table(chunk_cost, seq_len // align)
+    sv = _serving(fixed_cost, kv_bytes_per_token, stage_capacity, pairing, max_batch, requests)
+    ln = (ctypes.c_int32 * num_chunks)(*[int(x) for x in lengths])
+    b, pre, t = ctypes.c_int32(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(load_library().mocap_lbcp_evaluate(int(seq_len), int(num_chunks), int(num_stages), int(align), ptr,
+                                              ctypes.byref(sv), ln, ctypes.byref(b), ctypes.byref(pre),
+                                              ctypes.byref(t)), "mocap_lbcp_evaluate")
+    return b.value, pre.value, t.value
+
+
+def mocap_lbcp_refine_e2e(seq_len: int, num_chunks: int, num_stages: int, align: int, chunk_cost,
+                          lengths: Sequence[int], fixed_cost: float, kv_bytes_per_token: float,
+                          stage_capacity: float, pairing: bool, max_batch: int, requests: int,
+                          temp0: float, temp_min: float, alpha: float, rounds: int, seed: int):
+    """Returns (lengths, B', T'_pre, T') of the best partition the annealing found."""
+    arr, ptr = _cost_table(chunk_cost, seq_len // align)
+    sv = _serving(fixed_cost, kv_bytes_per_token, stage_capacity, pairing, max_batch, requests)
+    io = (ctypes.c_int32 * num_chunks)(*[int(x) for x in lengths])
+    b, pre, t = ctypes.c_int32(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(load_library().mocap_lbcp_refine_e2e(
+        int(seq_len), int(num_chunks), int(num_stages), int(align), ptr, ctypes.byref(sv), float(temp0),
+        float(temp_min), float(alpha), int(rounds), int(seed) & 0xFFFFFFFFFFFFFFFF, io, ctypes.byref(b),
+        ctypes.byref(pre), ctypes.byref(t)), "mocap_lbcp_refine_e2e")
+    return list(io), b.value, pre.value, t.value

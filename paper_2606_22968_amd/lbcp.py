@@ -20,6 +20,13 @@ balanced plan:
 With --layer, EvaluateChunk is the latency of a whole decoder layer per chunk
 (projections and feed-forward network included, layer.py), so both terms of
 Eq. (1) enter the model.
+
+With --stage2 the command also measures a (length, prefix) grid, builds a
+chunk-cost table and runs the second stage of Alg. 1 (mocap_lbcp_refine, the
+single-request refinement); --e2e adds the serving model of the second stage
+(mocap_lbcp_refine_e2e: the feasible batch under per-stage KV capacity, with
+and without the cross-half pairing of Section 4.1, and the end-to-end
+latency of a queue of requests) for several capacities.
 """
 import argparse
 import json
@@ -266,6 +273,39 @@ def cost_table(grid, model: LatencyModel, seq_len: int, align: int):
     return table
 
 
+def serving_study(table, start, model, seq_len, num_chunks, num_stages, align, h_kv, head_dim,
+                  layers_per_stage, requests, max_batch, capacities, seed):
+    """The table's plan against the annealed plan under the serving model
+    (mocap_lbcp_evaluate / mocap_lbcp_refine_e2e), per capacity and pairing.
+    A stage runs layers_per_stage layers: its chunk cost is that many times
+    the table's, its fixed per-chunk cost that many times the fitted
+    per-chunk constant, and a request token holds 2 h_kv d bf16 values per
+    layer on it."""
+    stage_table = table * layers_per_stage
+    e = model.cost_chunk * layers_per_stage
+    kv = float(layers_per_stage * 2 * h_kv * head_dim * 2)
+    one = seq_len * kv
+    out = []
+    for cap_units in capacities:
+        for pairing in (False, True):
+            args = (seq_len, num_chunks, num_stages, align, stage_table)
+            model_args = dict(fixed_cost=e, kv_bytes_per_token=kv, stage_capacity=cap_units * one,
+                              pairing=pairing, max_batch=max_batch, requests=requests)
+            b0, pre0, t0 = binding.mocap_lbcp_evaluate(*args, start, **model_args)
+            temp0 = 0.05 * t0 if t0 < float("inf") else 1e3
+            lengths, b1, pre1, t1 = binding.mocap_lbcp_refine_e2e(*args, start, **model_args, temp0=temp0,
+                                                                   temp_min=2e-3 * temp0, alpha=0.9, rounds=30,
+                                                                   seed=seed)
+            out.append({"capacity_requests": cap_units, "pairing": pairing,
+                        "dp": {"batch": b0, "t_pre_us": round(pre0, 1), "e2e_us": round(t0, 1)},
+                        "annealed": {"batch": b1, "t_pre_us": round(pre1, 1), "e2e_us": round(t1, 1),
+                                     "lengths": lengths, "left_dp_plan": list(lengths) != list(start)}})
+            print(f"[lbcp] e2e capacity {cap_units} pairing {pairing}: B {b0} -> {b1}, "
+                  f"T {t0 / 1e3:.1f} -> {t1 / 1e3:.1f} ms", file=sys.stderr, flush=True)
+    return {"requests": requests, "layers_per_stage": layers_per_stage, "fixed_cost_us": round(e, 1),
+            "kv_bytes_per_token_per_stage": kv, "max_batch": max_batch, "runs": out}
+
+
 def _objective(latencies: Sequence[float], num_stages: int) -> float:
     return sum(latencies) + (num_stages - 1) * max(latencies)
 
@@ -289,6 +329,17 @@ def main(argv=None):
                     help="also build a measured chunk-cost table over a (length, prefix) grid, run the "
                          "table-driven dynamic program and the simulated-annealing refinement, and "
                          "measure their plans")
+    ap.add_argument("--e2e", action="store_true",
+                    help="with --stage2: also refine the table's plan under the serving model "
+                         "(feasible batch under per-stage KV capacity, with and without cross-half pairing, "
+                         "and the workload's end-to-end latency) for several capacities")
+    ap.add_argument("--layers-per-stage", type=int, default=2,
+                    help="decoder layers per pipeline stage: scales the table, the fixed per-chunk cost and "
+                         "the KV bytes per token of a stage")
+    ap.add_argument("--requests", type=int, default=64, help="requests queued for the end-to-end latency")
+    ap.add_argument("--max-batch", type=int, default=16)
+    ap.add_argument("--capacities", default="2.25,3.5,5,7",
+                    help="per-stage KV capacities, in units of one request's KV on a stage")
     args = ap.parse_args(argv)
 
     w = synth.WORKLOADS[args.workload]
@@ -328,6 +379,11 @@ def main(argv=None):
         stage2 = {"grid_points": len(grid), "table_dp_model_us": round(t0, 1),
                   "refined_model_us": round(sa_lat, 1)}
         plans += [table_lengths, sa_lengths]
+        if args.e2e:
+            stage2["e2e"] = serving_study(table, table_lengths, model, seq_len, m, args.stages, align,
+                                          w.h_kv, w.head_dim, args.layers_per_stage, args.requests,
+                                          args.max_batch, [float(x) for x in args.capacities.split(",")],
+                                          w.seed)
     print("[lbcp] measuring the candidate plans", file=sys.stderr, flush=True)
     final = timed(plans)
 
