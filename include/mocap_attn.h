@@ -35,7 +35,13 @@
  *   - Position p of the sequence lives in logical block p / block_size at
  *     slot p % block_size; block_table[logical] gives the physical block.
  *     Table entries are trusted: each must lie in [0, num_blocks), and
- *     distinct positions must not share a slot.
+ *     distinct positions must not share a slot.  mocap_check_block_table
+ *     checks a host copy of a table; a library built with
+ *     -DMOCAP_DEBUG_TABLES (build.py --debug-tables, libmocap_attn_debug.so)
+ *     copies the entries each call will use to the host (a synchronous
+ *     copy, so such a build cannot be used under graph capture) and returns
+ *     MOCAP_ERR_INVALID_ARG, launching nothing, when one is out of range or
+ *     two logical blocks share a physical block.
  *   - All device pointers must be 16-byte aligned.
  */
 #ifndef MOCAP_ATTN_H
@@ -317,6 +323,24 @@ mocap_status mocap_lbcp_plan_table(int64_t seq_len, int32_t num_chunks, int32_t 
 mocap_status mocap_lbcp_refine(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
                                const double* chunk_cost, double temp0, double temp_min, double alpha,
                                int32_t rounds, uint64_t seed, int32_t* lengths_inout, double* latency_out);
+
+/*
+ * mocap_check_block_table -- check the entries of a block table (a HOST copy)
+ * that positions [first_pos, end_pos) use: logical blocks first_pos /
+ * block_size .. ceil(end_pos / block_size) - 1 must each name a physical
+ * block in [0, num_blocks), and no two of them the same one (Section 4.1's
+ * reallocation moves blocks; a table that maps two logical blocks onto one
+ * physical block would make appends overwrite each other).  Host only.
+ *
+ *   block_table    host int32 [n_table]
+ *   bad_index_out  (may be NULL) the first offending logical block, or -1
+ * Returns MOCAP_OK, or MOCAP_ERR_INVALID_ARG for a bad entry, a table shorter
+ * than the range needs, a null table for a non-empty range, or malformed
+ * sizes.
+ */
+mocap_status mocap_check_block_table(const int32_t* block_table, int32_t n_table, int64_t first_pos,
+                                     int64_t end_pos, int32_t block_size, int32_t num_blocks,
+                                     int32_t* bad_index_out);
 
 /*
  * The serving model of mocap_lbcp_evaluate and mocap_lbcp_refine_e2e: the

@@ -39,6 +39,7 @@ EXPORTED = (
     "mocap_lbcp_evaluate",
     "mocap_lbcp_refine_e2e",
     "mocap_status_string",
+    "mocap_check_block_table",
 )
 
 
@@ -71,6 +72,16 @@ class mocap_kv_store(ctypes.Structure):
 
 
 _lib = None
+
+# Debug option: check the block-table entries every call will use (a host copy,
+# so each call synchronises) before calling the library.
+_check_tables = os.environ.get("MOCAP_CHECK_TABLES", "0") == "1"
+
+
+def set_table_checks(enabled: bool) -> None:
+    """Turn the host-side block-table check of every call on or off."""
+    global _check_tables
+    _check_tables = bool(enabled)
 
 
 def load_library():
@@ -141,6 +152,10 @@ def load_library():
         ctypes.POINTER(mocap_lbcp_serving), ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32,
         ctypes.c_uint64, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    lib.mocap_check_block_table.restype = st
+    lib.mocap_check_block_table.argtypes = [
+        ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+        ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
     lib.mocap_chunk_plan.restype = st
     lib.mocap_chunk_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -198,6 +213,27 @@ class KvStore:
                               self.block_size, self.h_kv, self.head_dim)
 
 
+def mocap_check_block_table(block_table, first_pos: int, end_pos: int, block_size: int, num_blocks: int) -> None:
+    """Checks the entries positions [first_pos, end_pos) use (a host copy of
+    the table is taken if it lives on the GPU); raises MocapError, with
+    .bad_index, if one is out of range or repeats a physical block."""
+    t = block_table.detach().to("cpu", torch.int32).contiguous() if isinstance(block_table, torch.Tensor) \
+        else torch.tensor(list(block_table), dtype=torch.int32)
+    bad = ctypes.c_int32(-1)
+    st = load_library().mocap_check_block_table(
+        ctypes.cast(t.data_ptr(), ctypes.POINTER(ctypes.c_int32)), t.numel(), int(first_pos), int(end_pos),
+        int(block_size), int(num_blocks), ctypes.byref(bad))
+    if st != MOCAP_OK:
+        err = MocapError(st, f"mocap_check_block_table (logical block {bad.value})")
+        err.bad_index = bad.value
+        raise err
+
+
+def _maybe_check(store: "KvStore", block_table: torch.Tensor, first: int, end: int) -> None:
+    if _check_tables and end > first:
+        mocap_check_block_table(block_table, first, end, store.block_size, store.num_blocks)
+
+
 def mocap_kv_append(store: KvStore, block_table: torch.Tensor, start_pos: int,
                     k_chunk: torch.Tensor, v_chunk: torch.Tensor, stream=None) -> None:
     _require(block_table, torch.int32, "block_table", 1)
@@ -205,6 +241,7 @@ def mocap_kv_append(store: KvStore, block_table: torch.Tensor, start_pos: int,
     _require(v_chunk, torch.bfloat16, "v_chunk", 3)
     if k_chunk.shape != v_chunk.shape or tuple(k_chunk.shape[1:]) != (store.h_kv, store.head_dim):
         raise ValueError("k_chunk/v_chunk must be [chunk_len][h_kv][head_dim] of the store")
+    _maybe_check(store, block_table, int(start_pos), int(start_pos) + k_chunk.shape[0])
     desc = store.descriptor()
     _check(load_library().mocap_kv_append(
         ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), int(start_pos),
@@ -239,6 +276,7 @@ def mocap_chunk_attn(store: KvStore, block_table: torch.Tensor, q: torch.Tensor,
     if workspace is not None:
         _require(workspace, workspace.dtype, "workspace")
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    _maybe_check(store, block_table, 0, int(prefix_len) + chunk_len)
     desc = store.descriptor()
     _check(load_library().mocap_chunk_attn(
         ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), q.data_ptr(),
@@ -258,6 +296,7 @@ def mocap_chunk_attn_noalloc(store: KvStore, block_table: torch.Tensor, q: torch
     chunk_len, h_q, head_dim = q.shape
     if o.shape != q.shape or tuple(lse.shape) != (h_q, chunk_len):
         raise ValueError("o must match q and lse must be [h_q][chunk_len]")
+    _maybe_check(store, block_table, 0, int(prefix_len) + chunk_len)
     desc = store.descriptor()
     _check(load_library().mocap_chunk_attn_noalloc(
         ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), q.data_ptr(),
@@ -301,6 +340,12 @@ def mocap_chunk_attn_two_store(store: KvStore, block_table: torch.Tensor, remote
     if workspace is not None:
         _require(workspace, workspace.dtype, "workspace")
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    if int(remote_end) > int(remote_begin) and remote is not None:
+        _maybe_check(store, block_table, 0, int(remote_begin))
+        _maybe_check(store, block_table, int(remote_end), int(prefix_len) + chunk_len)
+        _maybe_check(remote, remote_table, int(remote_begin), int(remote_end))
+    else:
+        _maybe_check(store, block_table, 0, int(prefix_len) + chunk_len)
     desc = store.descriptor()
     _check(load_library().mocap_chunk_attn_two_store(
         ctypes.byref(desc), block_table.data_ptr(), block_table.numel(), r_desc, r_table, r_n,

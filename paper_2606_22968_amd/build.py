@@ -69,5 +69,18 @@ def _check_stubs(lib: str) -> None:
         raise RuntimeError("kernel launch stubs missing from " + lib + ":\n" + "\n".join(missing))
 
 
+DEBUG_LIB = os.path.join(PKG, "libmocap_attn_debug.so")
+
+
+def build_debug(verbose: bool = False) -> str:
+    """The library with host-side block-table checks before every launch
+    (-DMOCAP_DEBUG_TABLES): libmocap_attn_debug.so, for debugging callers."""
+    return build(verbose, extra_flags=("-DMOCAP_DEBUG_TABLES",), lib_path=DEBUG_LIB,
+                 build_dir=os.path.join(BUILD_DIR, "debug"))
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--debug-tables" in sys.argv:
+        print(build_debug(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))

@@ -12,6 +12,7 @@
 #include <functional>
 #include <mutex>
 #include <queue>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -332,6 +333,58 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   return MOCAP_OK;
 }
 
+// Host-side check of the block-table entries that positions [first, end) use:
+// each in [0, num_blocks), no two logical blocks on one physical block.
+mocap_status check_table_entries(const int32_t* table, int32_t n_table, int64_t first, int64_t end,
+                                 int32_t block_size, int32_t num_blocks, int32_t* bad_out) {
+  if (bad_out) *bad_out = -1;
+  if (first < 0 || end < first || block_size <= 0 || num_blocks <= 0 || n_table < 0) return MOCAP_ERR_INVALID_ARG;
+  if (end == first) return MOCAP_OK;
+  const int64_t b0 = first / block_size, b1 = (end + block_size - 1) / block_size;
+  if (b1 > n_table || table == nullptr) return MOCAP_ERR_INVALID_ARG;
+  std::vector<std::pair<int32_t, int64_t>> used;
+  used.reserve((size_t)(b1 - b0));
+  for (int64_t b = b0; b < b1; ++b) {
+    if (table[b] < 0 || table[b] >= num_blocks) {
+      if (bad_out) *bad_out = (int32_t)b;
+      return MOCAP_ERR_INVALID_ARG;
+    }
+    used.emplace_back(table[b], b);
+  }
+  std::sort(used.begin(), used.end());
+  for (size_t i = 1; i < used.size(); ++i) {
+    if (used[i].first == used[i - 1].first) {
+      if (bad_out) *bad_out = (int32_t)used[i].second;
+      return MOCAP_ERR_INVALID_ARG;
+    }
+  }
+  return MOCAP_OK;
+}
+
+// In a build with MOCAP_DEBUG_TABLES, every call copies the table entries it
+// will use to the host (a synchronous copy) and checks them before anything
+// is enqueued; a bad entry returns MOCAP_ERR_INVALID_ARG.
+#ifdef MOCAP_DEBUG_TABLES
+mocap_status debug_check_table(const int32_t* dev_table, int64_t first, int64_t end, const mocap_kv_store* kv) {
+  if (end <= first) return MOCAP_OK;
+  const int64_t b0 = first / kv->block_size, b1 = (end + kv->block_size - 1) / kv->block_size;
+  std::vector<int32_t> host((size_t)b1, 0);
+  if (hipMemcpy(host.data() + b0, dev_table + b0, (size_t)(b1 - b0) * sizeof(int32_t), hipMemcpyDeviceToHost) !=
+      hipSuccess)
+    return MOCAP_ERR_HIP;
+  return check_table_entries(host.data(), (int32_t)b1, first, end, kv->block_size, kv->num_blocks, nullptr);
+}
+#define MOCAP_DEBUG_CHECK(table, first, end, kv)                              \
+  do {                                                                        \
+    const mocap_status debug_st_ = debug_check_table((table), (first), (end), (kv)); \
+    if (debug_st_ != MOCAP_OK) return debug_st_;                              \
+  } while (0)
+#else
+#define MOCAP_DEBUG_CHECK(table, first, end, kv) \
+  do {                                           \
+  } while (0)
+#endif
+
 // ---- Scratch of the allocation-free entry point ----
 // Split partials of mocap_chunk_attn_noalloc live in this array: every device
 // the library runs on holds its own copy until the process ends.  Host code
@@ -386,6 +439,7 @@ mocap_status mocap_kv_append(const mocap_kv_store* kv, const int32_t* block_tabl
   if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || !aligned16(block_table) ||
       !aligned16(k_chunk) || !aligned16(v_chunk))
     return MOCAP_ERR_INVALID_ARG;
+  MOCAP_DEBUG_CHECK(block_table, start_pos, start_pos + chunk_len, kv);
 
   mocap::AppendLaunch p;
   p.k_chunk = static_cast<const uint16_t*>(k_chunk);
@@ -431,11 +485,18 @@ mocap_status mocap_chunk_attn(const mocap_kv_store* kv, const int32_t* block_tab
   mocap_status st = check_attn_args(kv, block_table, n_table, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
                                     scale, o, lse, num_splits);
   if (st != MOCAP_OK || chunk_len == 0) return st;
+  MOCAP_DEBUG_CHECK(block_table, 0, prefix_len + chunk_len, kv);
   Plan plan;
   st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
   if (st != MOCAP_OK) return st;
   return enqueue_attention(kv, block_table, nullptr, nullptr, plan, q, prefix_len, chunk_len, h_q, h_kv,
                            head_dim, scale, o, lse, workspace, workspace_bytes, stream);
+}
+
+mocap_status mocap_check_block_table(const int32_t* block_table, int32_t n_table, int64_t first_pos,
+                                     int64_t end_pos, int32_t block_size, int32_t num_blocks,
+                                     int32_t* bad_index_out) {
+  return check_table_entries(block_table, n_table, first_pos, end_pos, block_size, num_blocks, bad_index_out);
 }
 
 mocap_status mocap_chunk_attn_noalloc(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
@@ -445,6 +506,7 @@ mocap_status mocap_chunk_attn_noalloc(const mocap_kv_store* kv, const int32_t* b
   mocap_status st = check_attn_args(kv, block_table, n_table, q, prefix_len, chunk_len, h_q, h_kv, head_dim,
                                     scale, o, lse, num_splits);
   if (st != MOCAP_OK || chunk_len == 0) return st;
+  MOCAP_DEBUG_CHECK(block_table, 0, prefix_len + chunk_len, kv);
   Plan plan;
   st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan, kScratchBytes);
   if (st != MOCAP_OK) return st;
@@ -494,6 +556,7 @@ mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t*
   if (!valid_remote_range(remote_begin, remote_end, prefix_len)) return MOCAP_ERR_INVALID_ARG;
   if (remote_begin == remote_end) {
     if (chunk_len == 0) return MOCAP_OK;
+    MOCAP_DEBUG_CHECK(block_table, 0, prefix_len + chunk_len, kv);
     Plan plan;
     st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
     if (st != MOCAP_OK) return st;
@@ -511,6 +574,9 @@ mocap_status mocap_chunk_attn_two_store(const mocap_kv_store* kv, const int32_t*
   if (!remote_kv->k_pool || !remote_kv->v_pool || !remote_table || !aligned16(remote_kv->k_pool) ||
       !aligned16(remote_kv->v_pool) || !aligned16(remote_table))
     return MOCAP_ERR_INVALID_ARG;
+  MOCAP_DEBUG_CHECK(block_table, 0, remote_begin, kv);
+  MOCAP_DEBUG_CHECK(block_table, remote_end, prefix_len + chunk_len, kv);
+  MOCAP_DEBUG_CHECK(remote_table, remote_begin, remote_end, remote_kv);
   Plan plan;
   st = make_plan(prefix_len, chunk_len, h_q, h_kv, head_dim, num_splits, &plan);
   if (st != MOCAP_OK) return st;
