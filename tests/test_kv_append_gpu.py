@@ -24,6 +24,8 @@ def gather(store, table, seq_len):
     (8, 128, 256, [2048, 2048, 1024]),
     (2, 64, 64, [13, 100, 1, 129, 64, 77]),
     (4, 128, 128, [5, 300, 211]),
+    (2, 64, 64, [32, 96, 160, 7, 25]),          # 32-aligned starts inside 64-slot blocks
+    (8, 128, 256, [2080, 32, 2016, 33]),
 ])
 def test_gather_is_bit_exact(gpu, permuted, h_kv, d, bs, lengths):
     say(f"[case] append h_kv={h_kv} d={d} bs={bs} permuted={permuted}")
