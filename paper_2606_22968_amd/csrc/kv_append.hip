@@ -19,10 +19,13 @@
 // one barrier the tile leaves as 16-byte stores of 8 consecutive slots of one
 // head-dim row (a whole 32-aligned tile), or 2-byte stores at ragged edges.
 //
-// LDS tile: row e holds the 32 positions of dim e (64 bytes); the 16-byte
-// chunk q of row e (positions 8q .. 8q+7) is stored at chunk q ^ ((e / 8) % 4),
-// so the 16 lanes that one 16-byte read instruction serves at a time hit
-// distinct banks.
+// LDS tile: 16-byte chunk (e, q) holds positions 8q .. 8q+7 of dim e and is
+// stored at chunk slot (4 e + q) ^ ((e / 8) % 16).  For D = 128 a 2-byte
+// write instruction (16 chunk columns ch, dims e = 8 ch + k, positions
+// t, t+2, t+4, t+6) then lands in 16 distinct groups of four banks, one
+// dword of each bank, and the 16 lanes that a 16-byte read serves at a time
+// (chunks 16 m .. 16 m + 15) stay in distinct groups too: no bank conflicts.
+// (D = 64 has 8 chunk columns and writes two lanes per bank.)
 #include "internal.h"
 
 namespace mocap {
@@ -30,12 +33,15 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kAppendTokens = 32;  // positions per workgroup
+constexpr int kAppendTokens = 32;  // positions per workgroup (4 chunks of 8 per dim row)
 
 template <int D>
 constexpr int append_threads() { return kAppendTokens * (D / 8); }
 
-__device__ __forceinline__ int v_slot(int e, int tok) { return tok ^ (((e >> 3) & 3) << 3); }
+// Element index of (dim e, position tok) in the tile.
+__device__ __forceinline__ int v_index(int e, int tok) {
+  return ((((e << 2) + (tok >> 3)) ^ ((e >> 3) & 15)) << 3) + (tok & 7);
+}
 
 template <int D>
 __global__ __launch_bounds__(append_threads<D>()) void kv_append_kernel(const AppendLaunch p) {
@@ -56,9 +62,13 @@ __global__ __launch_bounds__(append_threads<D>()) void kv_append_kernel(const Ap
   const int64_t phys0 = p.table[lb0];
   const int64_t phys1 = split < n_tok ? (int64_t)p.table[lb0 + 1] : phys0;
 
-  // Thread -> (position, chunk): the D / 8 threads of a position read its
-  // whole K and V rows, consecutive 16-byte pieces.
-  const int tok = tid / ROW_CHUNKS, ch = tid % ROW_CHUNKS;
+  // Thread -> (position, chunk): the D / 8 lanes of a position read its
+  // whole K and V rows, consecutive 16-byte pieces.  A wavefront takes every
+  // other position of 2 * PW consecutive ones (wave pairs share them), so its
+  // 2-byte tile writes cover all four dwords of each 16-byte chunk.
+  constexpr int PW = 64 / ROW_CHUNKS;  // positions per wavefront
+  const int wv = tid >> 6, wl = tid & 63;
+  const int tok = (wv >> 1) * 2 * PW + (wv & 1) + 2 * (wl / ROW_CHUNKS), ch = wl % ROW_CHUNKS;
   if (tok < n_tok) {
     const int64_t src = ((int64_t)(t0 + tok) * p.h_kv + h) * D + ch * 8;
     const u32x4 kr = *reinterpret_cast<const u32x4*>(p.k_chunk + src);
@@ -69,8 +79,8 @@ __global__ __launch_bounds__(append_threads<D>()) void kv_append_kernel(const Ap
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const int e = ch * 8 + 2 * w;
-      vt[e * T + v_slot(e, tok)] = (uint16_t)(vr[w] & 0xFFFFu);
-      vt[(e + 1) * T + v_slot(e + 1, tok)] = (uint16_t)(vr[w] >> 16);
+      vt[v_index(e, tok)] = (uint16_t)(vr[w] & 0xFFFFu);
+      vt[v_index(e + 1, tok)] = (uint16_t)(vr[w] >> 16);
     }
   }
   __syncthreads();
@@ -80,7 +90,7 @@ __global__ __launch_bounds__(append_threads<D>()) void kv_append_kernel(const Ap
     // q), 8 consecutive slots of one head-dim row per 16-byte store.
     uint16_t* base = p.v_pool + (phys0 * p.h_kv + h) * D * (int64_t)p.block_size + slot00;
     const int e = tid / (T / 8), q = tid % (T / 8);
-    const u32x4 out = *reinterpret_cast<const u32x4*>(vt + e * T + v_slot(e, q * 8));
+    const u32x4 out = *reinterpret_cast<const u32x4*>(vt + v_index(e, q * 8));
     *reinterpret_cast<u32x4*>(base + (int64_t)e * p.block_size + q * 8) = out;
     return;
   }
@@ -90,7 +100,7 @@ __global__ __launch_bounds__(append_threads<D>()) void kv_append_kernel(const Ap
     const int64_t phys = lt < split ? phys0 : phys1;
     const int64_t slot = lt < split ? slot00 + lt : lt - split;
     uint16_t* dst = p.v_pool + (phys * p.h_kv + h) * D * (int64_t)p.block_size + slot;
-    for (int e = lr; e < D; e += NT / T) dst[(int64_t)e * p.block_size] = vt[e * T + v_slot(e, lt)];
+    for (int e = lr; e < D; e += NT / T) dst[(int64_t)e * p.block_size] = vt[v_index(e, lt)];
   }
 }
 
