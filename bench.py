@@ -27,6 +27,11 @@ Usage: python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-base
        python bench.py --summarize-trace KERNEL_TRACE_CSV [--steps K] [--workload NAME]
            (summary of the attention launches of the timed steps in a
             rocprofv3 --kernel-trace run of this script)
+       python bench.py --summarize-counters DIR --copy-calibration-mib M [--steps K] [--workload NAME]
+           (summary of three rocprofv3 --pmc runs of this script with
+            --copy-calibration-mib, written under DIR/fetch (FETCH_SIZE),
+            DIR/write (WRITE_SIZE) and DIR/sq (GRBM_GUI_ACTIVE and SQ
+            counters); writes profiles/chunk_attn_<workload>_counters.json)
 """
 import argparse
 import json
@@ -57,6 +62,8 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=8, help="oracle sample rows per (chunk, head)")
     ap.add_argument("--summarize-trace", default=None,
                     help="print a summary of a rocprofv3 kernel trace of this script and exit")
+    ap.add_argument("--summarize-counters", default=None,
+                    help="summarize rocprofv3 --pmc runs of this script (see usage) and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel for scaling a profiler's FETCH_SIZE / WRITE_SIZE counters)")
@@ -168,10 +175,141 @@ def summarize_trace(path, workload, steps):
     print("per-chunk median us: " + ", ".join(f"{x:.1f}" for x in per_chunk))
 
 
+XCDS = 8  # MI355X: GRBM_GUI_ACTIVE is reported summed over the 8 accelerator complex dies
+
+
+def _counter_rows(path):
+    """Rows of a rocprofv3 counter_collection.csv as (dispatch id, kernel,
+    counter, value, start ns, end ns)."""
+    import csv
+    out = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            out.append((int(r["Dispatch_Id"]), r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"]),
+                        int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    return out
+
+
+def _per_dispatch(rows, match):
+    """{dispatch id: (kernel, {counter: value}, start, end)} for kernels whose name contains `match`."""
+    d = {}
+    for did, name, ctr, val, t0, t1 in rows:
+        if match in name:
+            d.setdefault(did, (name, {}, t0, t1))[1][ctr] = val
+    return dict(sorted(d.items()))
+
+
+def summarize_counters(root, workload, steps, calib_mib):
+    """HBM bytes and average clock of the attention launches of the timed
+    steps, from rocprofv3 --pmc runs of this script (one run per counter
+    group, each with --copy-calibration-mib).  FETCH_SIZE and WRITE_SIZE are
+    scaled so that the calibration copy (the largest device copy of the run)
+    reads and writes its known size; the clock is the least-squares slope of
+    GRBM_GUI_ACTIVE per die against each launch's duration, which removes the
+    fixed per-dispatch part of the counter window."""
+    import glob
+    import hashlib
+    from paper_2606_22968_amd import binding, synth
+    w = synth.WORKLOADS[workload]
+    lengths = binding.mocap_chunk_plan(w.seq_len, w.num_chunks, w.align, balanced=(w.chunking == "balanced"))
+    n = steps * len(lengths)
+
+    def load(sub):
+        files = glob.glob(os.path.join(root, sub, "**", "*counter_collection.csv"), recursive=True)
+        if len(files) != 1:
+            raise SystemExit(f"{root}/{sub}: expected one counter_collection.csv, found {len(files)}")
+        rows = _counter_rows(files[0])
+        attn = list(_per_dispatch(rows, "chunk_attn_kernel").values())
+        if len(attn) < n:
+            raise SystemExit(f"{files[0]}: {len(attn)} attention launches, fewer than {steps} x {len(lengths)}")
+        copies = list(_per_dispatch(rows, "copyBuffer").values())
+        append = list(_per_dispatch(rows, "kv_append_kernel").values())
+        return attn[-n:], copies, append[-n:]
+
+    calib_bytes = None
+    scales, per_launch = {}, {}
+    for sub, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        attn, copies, append = load(sub)
+        # The calibration copy (the run's largest device copy) reads and
+        # writes calib_mib MiB.
+        big = max(copies, key=lambda c: c[1].get(ctr, 0.0))
+        kib = big[1][ctr]
+        calib_bytes = calib_mib * 2**20
+        scales[ctr] = calib_bytes / (kib * 1024)
+        per_launch[ctr] = statistics.mean(a[1][ctr] for a in attn) * 1024 * scales[ctr]
+        per_launch["append_" + ctr] = statistics.mean(a[1][ctr] for a in append) * 1024 * scales[ctr]
+    attn, _, append = load("sq")
+    dur = [(a[3] - a[2]) for a in attn]  # ns
+    cyc = [a[1]["GRBM_GUI_ACTIVE"] / XCDS for a in attn]
+    md, mc = statistics.mean(dur), statistics.mean(cyc)
+    slope = sum((d - md) * (c - mc) for d, c in zip(dur, cyc)) / sum((d - md) ** 2 for d in dur)
+    intercept = mc - slope * md
+    sums = {}
+    for a in attn:
+        for k, v in a[1].items():
+            sums[k] = sums.get(k, 0.0) + v
+    app = {}
+    for a in append:
+        for k, v in a[1].items():
+            app[k] = app.get(k, 0.0) + v
+    src = os.path.join(ROOT, "paper_2606_22968_amd", "csrc", "chunk_attn.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    rec = {
+        "kernel": attn[0][0],
+        "workload": workload,
+        "kernel_source_sha256": sha,
+        "launches": n,
+        "calibration_copy_bytes": calib_bytes,
+        "fetch_scale": scales["FETCH_SIZE"],
+        "write_scale": scales["WRITE_SIZE"],
+        "avg_fetch_bytes_per_launch": per_launch["FETCH_SIZE"],
+        "avg_write_bytes_per_launch": per_launch["WRITE_SIZE"],
+        "avg_traffic_bytes_per_launch": per_launch["FETCH_SIZE"] + per_launch["WRITE_SIZE"],
+        "avg_clock_ghz": round(slope, 4),
+        "clock_fit_intercept_cycles": round(intercept, 1),
+        "sq_totals": sums,
+        "kv_append": {
+            "kernel": append[0][0] if append else None,
+            "avg_fetch_bytes_per_launch": per_launch["append_FETCH_SIZE"],
+            "avg_write_bytes_per_launch": per_launch["append_WRITE_SIZE"],
+            "sq_totals": app,
+        },
+    }
+    out = os.path.join(ROOT, "profiles", f"chunk_attn_{workload}_counters.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    mfma = sums.get("SQ_INSTS_MFMA", 0.0)
+    busy_cycles = sum(cyc)
+    print(f"kernel: {rec['kernel']} ({n} launches of the timed step(s)); source sha256 {sha[:16]}")
+    print(f"calibration copy {calib_bytes / 2**20:.0f} MiB: FETCH_SIZE x {scales['FETCH_SIZE']:.4f}, "
+          f"WRITE_SIZE x {scales['WRITE_SIZE']:.4f}")
+    print(f"HBM bytes per launch: fetched {per_launch['FETCH_SIZE']:.4e}, written {per_launch['WRITE_SIZE']:.4e}, "
+          f"total {rec['avg_traffic_bytes_per_launch']:.4e}")
+    print(f"clock: {slope:.3f} GHz (slope of GRBM_GUI_ACTIVE / {XCDS} over duration; "
+          f"intercept {intercept:.0f} cycles per launch)")
+    for k in sorted(sums):
+        extra = f"  ({sums[k] / mfma:.2f} per MFMA)" if mfma and k.startswith("SQ_INSTS") else ""
+        print(f"  {k}: {sums[k]:.4e}{extra}")
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in sums and busy_cycles > 0:
+        # 4 SIMDs x 32 CUs per die: MFMA-busy cycles per SIMD over the die's active cycles.
+        print(f"MFMA unit busy: {sums['SQ_VALU_MFMA_BUSY_CYCLES'] / (busy_cycles * 1024):.3f} of active cycles")
+    if append:
+        print(f"kv_append ({len(append)} launches): fetched {per_launch['append_FETCH_SIZE']:.4e}, written "
+              f"{per_launch['append_WRITE_SIZE']:.4e} bytes per launch; "
+              + ", ".join(f"{k} {v:.4e}" for k, v in sorted(app.items())))
+    print(f"wrote {os.path.relpath(out, ROOT)}")
+
+
 def main():
     args = parse()
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.workload, args.steps)
+        return
+    if args.summarize_counters:
+        if args.copy_calibration_mib <= 0:
+            raise SystemExit("--summarize-counters needs the --copy-calibration-mib of the profiled runs")
+        summarize_counters(args.summarize_counters, args.workload, args.steps, args.copy_calibration_mib)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
