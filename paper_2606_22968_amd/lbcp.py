@@ -338,7 +338,7 @@ def main(argv=None):
                          "the KV bytes per token of a stage")
     ap.add_argument("--requests", type=int, default=64, help="requests queued for the end-to-end latency")
     ap.add_argument("--max-batch", type=int, default=16)
-    ap.add_argument("--capacities", default="2.25,3.5,5,7",
+    ap.add_argument("--capacities", default="2.5,4,5.5,7",
                     help="per-stage KV capacities, in units of one request's KV on a stage")
     args = ap.parse_args(argv)
 
