@@ -242,6 +242,19 @@ mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align
                               int32_t* lengths_out);
 
 /*
+ * mocap_chunk_prefixes -- prefix offsets of a chunk sequence (host only):
+ * prefixes_out[c] = lengths[0] + ... + lengths[c - 1], the number of earlier
+ * tokens every query of chunk c attends to (P_c above; Section 2.2, the p_i
+ * of Eq. (1)).
+ *
+ *   lengths       host int32 [num_chunks], each >= 0
+ *   prefixes_out  host int64 [num_chunks]; prefixes_out[0] = 0
+ * Errors: INVALID_ARG for num_chunks < 0, a negative length, or a null array
+ * with num_chunks > 0.
+ */
+mocap_status mocap_chunk_prefixes(const int32_t* lengths, int32_t num_chunks, int64_t* prefixes_out);
+
+/*
  * mocap_lbcp_plan -- first stage of latency-balanced chunk partitioning
  * (Section 4.2, Alg. 1, the dynamic-programming initialisation), host only.
  *

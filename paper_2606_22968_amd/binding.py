@@ -33,6 +33,7 @@ EXPORTED = (
     "mocap_chunk_attn_two_store",
     "mocap_chunk_attn_two_store_workspace_size",
     "mocap_chunk_plan",
+    "mocap_chunk_prefixes",
     "mocap_lbcp_plan",
     "mocap_lbcp_plan_table",
     "mocap_lbcp_refine",
@@ -160,6 +161,9 @@ def load_library():
     lib.mocap_chunk_plan.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
         ctypes.POINTER(ctypes.c_int32)]
+    lib.mocap_chunk_prefixes.restype = st
+    lib.mocap_chunk_prefixes.argtypes = [
+        ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]
     _lib = lib
     return lib
 
@@ -359,6 +363,14 @@ def mocap_chunk_plan(seq_len: int, num_chunks: int, align: int = 128, balanced: 
     _check(load_library().mocap_chunk_plan(int(seq_len), int(num_chunks), int(align), int(bool(balanced)), out),
            "mocap_chunk_plan")
     return list(out)
+
+
+def mocap_chunk_prefixes(lengths: Sequence[int]) -> List[int]:
+    n = len(lengths)
+    ln = (ctypes.c_int32 * max(n, 1))(*[int(x) for x in lengths])
+    out = (ctypes.c_int64 * max(n, 1))()
+    _check(load_library().mocap_chunk_prefixes(ln, n, out), "mocap_chunk_prefixes")
+    return list(out)[:n]
 
 
 def mocap_lbcp_plan(seq_len: int, num_chunks: int, num_stages: int, align: int, cost_pair: float,

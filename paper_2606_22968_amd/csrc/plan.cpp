@@ -405,6 +405,21 @@ mocap_status mocap_chunk_plan(int64_t seq_len, int32_t num_chunks, int32_t align
   return MOCAP_OK;
 }
 
+mocap_status mocap_chunk_prefixes(const int32_t* lengths, int32_t num_chunks, int64_t* prefixes_out) {
+  if (num_chunks < 0 || (num_chunks > 0 && (lengths == nullptr || prefixes_out == nullptr)))
+    return MOCAP_ERR_INVALID_ARG;
+  for (int c = 0; c < num_chunks; ++c)
+    if (lengths[c] < 0) return MOCAP_ERR_INVALID_ARG;
+  // P_c = L_0 + ... + L_{c-1}: at most 2^31 chunks of at most 2^31 - 1 tokens,
+  // so the sum stays below 2^62.
+  int64_t p = 0;
+  for (int c = 0; c < num_chunks; ++c) {
+    prefixes_out[c] = p;
+    p += lengths[c];
+  }
+  return MOCAP_OK;
+}
+
 mocap_status mocap_lbcp_plan(int64_t seq_len, int32_t num_chunks, int32_t num_stages, int32_t align,
                              double cost_pair, double cost_token, double cost_chunk,
                              int32_t* lengths_out, double* t_max_out, double* t_sum_out) {

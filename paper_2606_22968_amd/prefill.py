@@ -26,12 +26,8 @@ class ChunkedPrefill:
                  remote_table: Optional[torch.Tensor] = None):
         self.h_q, self.h_kv, self.head_dim = h_q, h_kv, head_dim
         self.lengths = [int(n) for n in lengths]
-        self.prefixes = []
-        acc = 0
-        for n in self.lengths:
-            self.prefixes.append(acc)
-            acc += n
-        self.seq_len = acc
+        self.prefixes = binding.mocap_chunk_prefixes(self.lengths)
+        self.seq_len = (self.prefixes[-1] + self.lengths[-1]) if self.lengths else 0
         self.block_size = block_size
         n_logical = (self.seq_len + block_size - 1) // block_size
         if table is None:

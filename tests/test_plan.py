@@ -90,3 +90,35 @@ def test_library_planner_rejects_bad_input(mocap_lib):
         mocap_lib.mocap_chunk_plan(3, 5, 1, balanced=False)       # empty chunks
     with pytest.raises(mocap_lib.MocapError):
         mocap_lib.mocap_chunk_plan(256, 4, 128, balanced=True)    # rounding leaves a chunk empty
+
+
+def test_oracle_prefixes_invariants():
+    # P_0 = 0, P_{c+1} = P_c + L_c, and the last prefix plus its chunk is S.
+    rng = random.Random(11)
+    for _ in range(20):
+        lengths = [rng.randint(0, 300) for _ in range(rng.randint(1, 40))]
+        p = plan.prefixes(lengths)
+        assert p[0] == 0
+        assert all(p[c + 1] == p[c] + lengths[c] for c in range(len(lengths) - 1))
+        assert p[-1] + lengths[-1] == sum(lengths)
+        # P_c counts the tokens that belong to earlier chunks, one by one.
+        owner = [c for c, n in enumerate(lengths) for _ in range(n)]
+        assert p == [sum(1 for o in owner if o < c) for c in range(len(lengths))]
+
+
+def test_library_prefixes_match_oracle(mocap_lib):
+    rng = random.Random(12)
+    cases = [[1], [0, 0, 3], plan.balanced_plan(131072, 16, 128), [2**31 - 1] * 5]
+    cases += [[rng.randint(0, 100000) for _ in range(rng.randint(1, 64))] for _ in range(10)]
+    for lengths in cases:
+        assert mocap_lib.mocap_chunk_prefixes(lengths) == plan.prefixes(lengths)
+    assert mocap_lib.mocap_chunk_prefixes([]) == []
+
+
+def test_library_prefixes_reject(mocap_lib):
+    with pytest.raises(mocap_lib.MocapError):
+        mocap_lib.mocap_chunk_prefixes([5, -1, 3])
+    lib = mocap_lib.load_library()
+    out = (mocap_lib.ctypes.c_int64 * 2)()
+    assert lib.mocap_chunk_prefixes(None, 2, out) == mocap_lib.MOCAP_ERR_INVALID_ARG
+    assert lib.mocap_chunk_prefixes(None, -1, out) == mocap_lib.MOCAP_ERR_INVALID_ARG
