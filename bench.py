@@ -58,6 +58,10 @@ def parse():
     ap.add_argument("--remote-fraction", type=float, default=0.0,
                     help="hold the KV of the first fraction of the sequence (whole blocks) in a second store, "
                          "as a debtor stage's remote portion, and read it with the two-store call")
+    ap.add_argument("--dominant-key", action="store_true",
+                    help="plant, for every KV head, one key of the last chunk at 8x a later query of that "
+                         "chunk, so that query's score sits ~130 binary orders above its first key block and "
+                         "the kernel raises that row's reference exponent and rescales it (times the data-dependent slow path)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8, help="oracle sample rows per (chunk, head)")
     ap.add_argument("--summarize-trace", default=None,
@@ -328,6 +332,14 @@ def main():
     w = synth.WORKLOADS[args.workload]
     lengths = binding.mocap_chunk_plan(w.seq_len, w.num_chunks, w.align, balanced=(w.chunking == "balanced"))
     q, k, v = synth.make_qkv(w.seed, w.seq_len, w.h_q, w.h_kv, w.head_dim)
+    planted = None
+    if args.dominant_key:
+        p_last = synth.prefixes(lengths)[-1]
+        key, row = p_last + 5, p_last + min(200, lengths[-1] - 1)
+        g = w.h_q // w.h_kv
+        for h in range(w.h_kv):
+            k[key, h] = (8.0 * q[row, h * g].float()).to(torch.bfloat16)
+        planted = {"key": key, "query_row": row}
     n_blocks = (w.seq_len + w.block_size - 1) // w.block_size
     table = synth.permuted_table(n_blocks, w.perm_seed) if w.permuted else None
     remote = None
@@ -403,6 +415,7 @@ def main():
             "block_size": w.block_size, "block_table": "permuted" if w.permuted else "identity",
             "split_plan": runner.splits,
             "remote_kv": list(runner.remote) if runner.remote else None,
+            "dominant_key": planted,
             "parallelism": "single GPU",
         },
         "pct_of_bf16_peak": round(100.0 * value / MFMA_BF16_PEAK_TFLOPS, 2),

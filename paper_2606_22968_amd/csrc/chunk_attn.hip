@@ -128,9 +128,10 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
 // the O accumulator never needs rescaling.  A later block whose partial row
 // sum exceeds kSumLimit = 2^60 (a score more than ~60 binary orders above the
 // first block's maximum, which ordinary attention scores never reach) marks
-// the row; after the pass the workgroup re-runs its key range once with m
-// raised to the largest such block maximum.  O is therefore only ever written
-// by MFMAs inside the loop.
+// the row: its m is raised to that block's maximum, its O accumulator and
+// row sums (all of earlier blocks, taken with the old m) are scaled by
+// 2^(m_old - m_new), and the block's probabilities are recomputed before
+// they reach the P*V product.  The loop itself never rescales.
 constexpr float kSumLimit = 1152921504606846976.0f;  // 2^60
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -197,8 +198,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   constexpr int STAGES = 4;
 
   __shared__ __attribute__((aligned(1024))) uint16_t lds[STAGES * BUF_ELEMS];
-  // Between passes no tile is in flight, so the re-run vote borrows LDS.
-  int* const rerun_flag = reinterpret_cast<int*>(lds);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -342,8 +341,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
   // l_run: sum of the bf16 probabilities (normalises O); f_run: sum of the
   // fp32 exponentials (the log-sum-exp).
-  float m_run = -INFINITY, l_run = 0.f, f_run = 0.f, m_cand = -INFINITY;
-  bool rerun = false;
+  float m_run = -INFINITY, l_run = 0.f, f_run = 0.f;
   const float sl2 = p.scale_log2;
   int k_row_lo = key_row_order(l32);
   int v_row_sw = v_swizzle(l32);
@@ -444,15 +442,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 #pragma unroll
         for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, s[sb][i2]);
       mx = lane_pair_max(mx) * sl2;
-      const bool fresh = lane_pair_sum(l_run) == 0.f;
-      if (row_over && !fresh) {
-        m_cand = fmaxf(m_cand, mx);
-        rerun = true;
-      }
-      if (row_over && fresh) {
+      if (row_over) {
+        // A row with nothing accumulated yet (m = -inf) just takes its
+        // reference; otherwise everything accumulated so far is rescaled.
+        if (lane_pair_sum(l_run) != 0.f) {
+          const float f = __builtin_amdgcn_exp2f(m_run - mx);
+#pragma unroll
+          for (int md = 0; md < MD; ++md) oacc[md] *= f;
+          l_run *= f;
+          f_run *= f;
+        }
         m_run = mx;
-        const float nm = m_run == -INFINITY ? 0.f : -m_run;
-        probs(b, nm);
+        probs(b, m_run == -INFINITY ? 0.f : -m_run);
       }
     }
     l_run += rs[0] + rs[1];
@@ -551,9 +552,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     settle(b);
   };
 
-  for (int pass = 0; pass < 2 && n_tiles > 0; ++pass) {
+  if (n_tiles > 0) {
     // Without this, values the first tile derives from these (its masks, its
-    // LDS addresses) are computed once before the pass loop and then occupy
+    // LDS addresses) are computed once ahead of the loop and then occupy
     // registers through every later tile.
     asm volatile("" : "+s"(lo), "+s"(hi), "+v"(k_row_lo), "+v"(v_row_sw));
     issue_seq(0);
@@ -581,21 +582,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       pv(n_w - 1, 0);
     }
     for (int i = max(n_w, 1); i < n_tiles; ++i) barrier_k(i);
-    lds_barrier();  // every wave is done with the tiles
-    if (tid == 0) *rerun_flag = 0;
-    lds_barrier();
-    if (pass == 0 && __builtin_amdgcn_ballot_w64(rerun) != 0 && lane == 0) atomicOr(rerun_flag, 1);
-    lds_barrier();
-    const bool again = *rerun_flag != 0;
-    lds_barrier();  // before the next pass's loads overwrite the flag
-    if (!again) break;
-    m_run = fmaxf(m_run, m_cand);
-    m_cand = -INFINITY;
-    l_run = 0.f;
-    f_run = 0.f;
-#pragma unroll
-    for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
-    rerun = false;
   }
 
   const bool split = p.n_ranges > 1;

@@ -96,10 +96,11 @@ def test_score_far_above_first_block_reruns(gpu, oracle_lib, target):
     # One late key is 8 * q for every query of the last chunk, so its score
     # is ~90 natural-log units (~130 binary orders) above anything in the
     # first key block: the kernel's reference exponent overflows and the
-    # workgroup re-runs its range.  The output must still match the oracle.
+    # kernel raises that row's reference exponent mid-range and rescales what
+    # it has accumulated.  The output must still match the oracle.
     lengths = [1024, 256]
     S = sum(lengths)
-    say(f"[case] overflow re-run, big key in the {target}")
+    say(f"[case] overflow rescale, big key in the {target}")
     q, k, v = synth.make_qkv(70, S, 8, 2, 128)
     j = 900 if target == "prefix" else 1024 + 5
     qf = q.float()
@@ -107,7 +108,7 @@ def test_score_far_above_first_block_reruns(gpu, oracle_lib, target):
         k[j, h_kv] = (8.0 * qf[1024 + 200, h_kv * 4]).to(torch.bfloat16)
     scale = 128 ** -0.5
     runner = run_gpu(q, k, v, lengths, scale)
-    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"overflow re-run ({target})")
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"overflow rescale ({target})")
 
 
 def _random_config(index):
