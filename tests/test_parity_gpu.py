@@ -111,6 +111,32 @@ def test_score_far_above_first_block_reruns(gpu, oracle_lib, target):
     check_chunks(oracle_lib, runner, q, k, v, scale, label=f"overflow rescale ({target})")
 
 
+@pytest.mark.parametrize("splits", [0, 1, 3])
+@pytest.mark.parametrize("d", [64, 128])
+def test_score_growing_over_several_blocks(gpu, oracle_lib, splits, d):
+    # For one query row per KV head, three keys in different key blocks score
+    # ~4, 8 and 12 times |q|^2 * scale: each one more than 60 binary orders
+    # above the one before, so the row's reference exponent is raised three
+    # times (the last time inside the chunk's own, masked, diagonal blocks),
+    # across split ranges when the prefix is split.  Other rows of the group
+    # see those keys at ordinary scores.
+    lengths = [700, 300, 260]
+    S = sum(lengths)
+    h_q, h_kv = 8, 2
+    g = h_q // h_kv
+    say(f"[case] growing scores d={d} splits={splits}")
+    q, k, v = synth.make_qkv(73 + d, S, h_q, h_kv, d)
+    qf = q.float()
+    row = 1000 + 200                      # a row of the last chunk
+    mult = 128.0 / d                      # the same score scale at d = 64
+    for h in range(h_kv):
+        for pos, c in ((150, 4.0), (820, 8.0), (1000 + 70, 12.0)):
+            k[pos + h, h] = (c * mult * qf[row + h, h * g]).to(torch.bfloat16)
+    scale = d ** -0.5
+    runner = run_gpu(q, k, v, lengths, scale, block_size=64, num_splits=splits)
+    check_chunks(oracle_lib, runner, q, k, v, scale, label=f"growing scores d={d} splits={splits}")
+
+
 def _random_config(index):
     """Seeded random shape: heads, head_dim, block size, chunk lengths, table
     and split count drawn independently (at most ~2500 tokens, 32 query heads)."""
