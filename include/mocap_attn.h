@@ -46,6 +46,11 @@
  *     MOCAP_ERR_INVALID_ARG, launching nothing, when one is out of range or
  *     two logical blocks share a physical block.
  *   - All device pointers must be 16-byte aligned.
+ *   - The attention calls choose, per launch and from a time model, how the
+ *     two halves of a workgroup pair up query rows; the environment variable
+ *     MOCAP_PAIRING=mirrored or =adjacent forces one choice (for testing).
+ *     Results agree with the oracle either way; they need not be bitwise
+ *     equal between the two.
  */
 #ifndef MOCAP_ATTN_H
 #define MOCAP_ATTN_H

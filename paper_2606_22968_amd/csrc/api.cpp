@@ -9,6 +9,8 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
+#include <cstring>
 #include <functional>
 #include <mutex>
 #include <queue>
@@ -102,7 +104,8 @@ constexpr double kLaunchUs = 4.0;
 constexpr double kLoneTile = 0.65;
 
 double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int head_dim, int head_blocks_total,
-                          int row_groups, int rows_per_unit, int64_t prefix_tiles, int n_ranges, int slots) {
+                          int row_groups, int rows_per_unit, int64_t prefix_tiles, int n_ranges, int slots,
+                          bool adjacent) {
   std::vector<double> cost;
   const int pairs = (row_groups + 1) / 2;
   cost.reserve((size_t)head_blocks_total * pairs * n_ranges);
@@ -114,8 +117,11 @@ double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int he
     return (prefix_len + row_end + kTileKeys - 1) / kTileKeys - t0;
   };
   for (int q = 0; q < pairs; ++q) {
-    const int64_t a = unit_tiles(q);
-    const int64_t b = q == row_groups - 1 - q ? 0 : unit_tiles(row_groups - 1 - q);
+    // Mirrored pair q: row groups q and R-1-q; adjacent pair q: R-2-2q and R-1-2q.
+    const int top = adjacent ? row_groups - 1 - 2 * q : row_groups - 1 - q;
+    const int other = adjacent ? top - 1 : q;
+    const int64_t a = unit_tiles(top);
+    const int64_t b = (other < 0 || other == top) ? 0 : unit_tiles(other);
     const double us = (double)std::min(a, b) * tile_us + (double)(std::max(a, b) - std::min(a, b)) * kLoneTile * tile_us;
     for (int hb = 0; hb < head_blocks_total; ++hb) cost.push_back(us + kGroupUs);
   }
@@ -144,13 +150,48 @@ double estimate_launch_us(int64_t prefix_len, int32_t chunk_len, int h_q, int he
   return total;
 }
 
+// 0 = automatic pairing choice; MOCAP_PAIRING=mirrored (1) or adjacent (2).
+int pairing_mode() {
+  const char* force = std::getenv("MOCAP_PAIRING");
+  if (force && std::strcmp(force, "mirrored") == 0) return 1;
+  if (force && std::strcmp(force, "adjacent") == 0) return 2;
+  return 0;
+}
+
+// The better of the two pairings of row groups in a workgroup (mirrored:
+// q with R-1-q, every workgroup about equally long, the shorter unit idle
+// for part of the diagonal; adjacent: 2q with 2q+1, both units busy nearly
+// throughout, workgroups of different lengths balanced by longest-first
+// scheduling when there are many per compute unit).  MOCAP_PAIRING=mirrored
+// or =adjacent in the environment forces one (for tests).
+double best_pairing_us(int64_t prefix_len, int32_t chunk_len, int h_q, int head_dim, int head_blocks_total,
+                       int row_groups, int rows_per_unit, int64_t prefix_tiles, int n_ranges, int slots,
+                       bool* adjacent_out) {
+  const int mode = pairing_mode();
+  const bool only_mirrored = mode == 1, only_adjacent = mode == 2;
+  const double mirrored = only_adjacent ? INFINITY
+                                        : estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total,
+                                                             row_groups, rows_per_unit, prefix_tiles, n_ranges, slots,
+                                                             false);
+  const double adjacent = only_mirrored ? INFINITY
+                                        : estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total,
+                                                             row_groups, rows_per_unit, prefix_tiles, n_ranges, slots,
+                                                             true);
+  // Adjacent only when the model expects it to win clearly.
+  const bool adj = only_adjacent || (!only_mirrored && adjacent < mirrored * 0.98);
+  if (adjacent_out) *adjacent_out = adj;
+  return adj ? adjacent : mirrored;
+}
+
 struct PlanKey {
   int64_t prefix_len;
   int32_t chunk_len, h_q, h_kv, head_dim, requested, slots;
   size_t ws_cap;
+  int pairing;
   bool operator==(const PlanKey& o) const {
     return prefix_len == o.prefix_len && chunk_len == o.chunk_len && h_q == o.h_q && h_kv == o.h_kv &&
-           head_dim == o.head_dim && requested == o.requested && slots == o.slots && ws_cap == o.ws_cap;
+           head_dim == o.head_dim && requested == o.requested && slots == o.slots && ws_cap == o.ws_cap &&
+           pairing == o.pairing;
   }
 };
 
@@ -176,20 +217,20 @@ int choose_ranges(int64_t prefix_len, int32_t chunk_len, int h_q, int h_kv, int 
     const int64_t parts = requested - 1 < prefix_tiles ? requested - 1 : prefix_tiles;
     return (int)parts + 1;
   }
-  const PlanKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, requested, slots, ws_cap};
+  const PlanKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, requested, slots, ws_cap, pairing_mode()};
   {
     std::lock_guard<std::mutex> lock(g_plan_mutex);
     for (int i = 0; i < g_plan_count; ++i)
       if (g_plan_keys[i] == key) return g_plan_values[i];
   }
   int best = 1;
-  double best_us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
-                                      rows_per_unit, prefix_tiles, 1, slots);
+  double best_us = best_pairing_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
+                                   rows_per_unit, prefix_tiles, 1, slots, nullptr);
   const int64_t max_parts = std::min<int64_t>(16, prefix_tiles / 4);
   for (int64_t parts = 1; parts <= max_parts; parts *= 2) {
     if (workspace_for((int)parts + 1, chunk_len, h_q, head_dim) > ws_cap) break;
-    const double us = estimate_launch_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
-                                         rows_per_unit, prefix_tiles, (int)parts + 1, slots);
+    const double us = best_pairing_us(prefix_len, chunk_len, h_q, head_dim, head_blocks_total, row_groups,
+                                      rows_per_unit, prefix_tiles, (int)parts + 1, slots, nullptr);
     if (us < best_us * 0.98) {  // a split must pay for itself clearly
       best_us = us;
       best = (int)parts + 1;
@@ -269,6 +310,40 @@ bool valid_remote_range(int64_t begin, int64_t end, int64_t prefix_len) {
   return begin >= 0 && begin <= end && end <= prefix_len && begin % kTileKeys == 0 && end % kTileKeys == 0;
 }
 
+// Pairing of row groups for a launch (best_pairing_us), cached per shape.
+struct PairKey {
+  int64_t prefix_len;
+  int32_t chunk_len, h_q, h_kv, head_dim, n_ranges, slots, mode;
+  bool operator==(const PairKey& o) const {
+    return prefix_len == o.prefix_len && chunk_len == o.chunk_len && h_q == o.h_q && h_kv == o.h_kv &&
+           head_dim == o.head_dim && n_ranges == o.n_ranges && slots == o.slots && mode == o.mode;
+  }
+};
+PairKey g_pair_keys[kPlanCache];
+bool g_pair_values[kPlanCache];
+int g_pair_count = 0, g_pair_next = 0;
+
+bool choose_pairing(const Plan& plan, int64_t prefix_len, int32_t chunk_len, int32_t h_q, int32_t h_kv,
+                    int32_t head_dim, int cus) {
+  if (plan.row_groups <= 2) return false;  // a single pair: both pairings are the same
+  const PairKey key{prefix_len, chunk_len, h_q, h_kv, head_dim, plan.n_ranges, cus, pairing_mode()};
+  {
+    std::lock_guard<std::mutex> lock(g_plan_mutex);
+    for (int i = 0; i < g_pair_count; ++i)
+      if (g_pair_keys[i] == key) return g_pair_values[i];
+  }
+  const int rows_per_unit = kAttnWaveRows * (kAttnWaves / 2 / plan.hu);
+  bool adjacent = false;
+  best_pairing_us(prefix_len, chunk_len, h_q, head_dim, h_q / plan.hu, plan.row_groups, rows_per_unit,
+                  plan.prefix_tiles, plan.n_ranges, std::max(cus, 1), &adjacent);
+  std::lock_guard<std::mutex> lock(g_plan_mutex);
+  g_pair_keys[g_pair_next] = key;
+  g_pair_values[g_pair_next] = adjacent;
+  g_pair_next = (g_pair_next + 1) % kPlanCache;
+  if (g_pair_count < kPlanCache) ++g_pair_count;
+  return adjacent;
+}
+
 // Launches the attention kernel (and the merge when the plan is split).
 // Arguments have been validated; remote_kv is used only for the plan's
 // second-store ranges.
@@ -302,6 +377,12 @@ mocap_status enqueue_attention(const mocap_kv_store* kv, const int32_t* block_ta
   p.heads_per_unit = plan.hu;
   p.row_groups = plan.row_groups;
   p.pairs = plan.pairs;
+  {
+    int cus = 0;
+    const mocap_status st = device_cu_count(&cus);
+    if (st != MOCAP_OK) return st;
+    p.pair_adjacent = choose_pairing(plan, prefix_len, chunk_len, h_q, h_kv, head_dim, cus) ? 1 : 0;
+  }
   p.block_size = kv->block_size;
   block_divider((uint32_t)kv->block_size, &p.block_magic, &p.block_shift);
   p.n_ranges = plan.n_ranges;

@@ -112,9 +112,16 @@ __device__ __forceinline__ WorkItem decode_item(const AttnLaunch& p, int hw_id) 
   r -= w.range * per_range;
   const int pair = r / head_blocks;
   const int hb = r - pair * head_blocks;
-  w.row_group_a = pair;
-  w.row_group_b = p.row_groups - 1 - pair;
-  if (w.row_group_b == pair) w.row_group_b = -1;
+  // Unit A takes the lower row group of the pair, unit B the higher (-1: none).
+  if (p.pair_adjacent) {
+    const int top = p.row_groups - 1 - 2 * pair;
+    w.row_group_a = top > 0 ? top - 1 : top;
+    w.row_group_b = top > 0 ? top : -1;
+  } else {
+    w.row_group_a = pair;
+    w.row_group_b = p.row_groups - 1 - pair;
+    if (w.row_group_b == pair) w.row_group_b = -1;
+  }
   w.head0 = w.kv_head * p.group + hb * p.heads_per_unit;
   return w;
 }

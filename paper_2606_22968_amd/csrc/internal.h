@@ -17,8 +17,10 @@ constexpr int kGroupThreads = 64 * kWavesPerGroup;
 // One launch of the attention kernel: every workgroup holds two units of four
 // wavefronts; a unit owns `heads_per_unit` query heads of one GQA group times
 // `32 * 4 / heads_per_unit` query rows (a row group).  The units of a
-// workgroup take row groups q and row_groups - 1 - q of the same heads (pair
-// q; the middle group of an odd count is alone), for one KV range.
+// workgroup take two row groups of the same heads, for one KV range: pair q
+// is row groups q and row_groups - 1 - q (mirrored; the middle group of an
+// odd count is alone), or row_groups - 2 - 2q and row_groups - 1 - 2q
+// (adjacent, longest pair first; group 0 alone when the count is odd).
 //
 // KV ranges: n_ranges == 1 is the unsplit launch over [0, P + L); otherwise
 // n_ranges - 1 ranges cut the prefix tiles [0, ceil(P / 64)) evenly (the
@@ -46,6 +48,7 @@ struct AttnLaunch {
   int32_t heads_per_unit;   // 2 or 1 (divides group)
   int32_t row_groups;       // ceil(L / rows_per_unit)
   int32_t pairs;            // ceil(row_groups / 2)
+  int32_t pair_adjacent;    // 0 = mirrored pairs, 1 = adjacent pairs
   int32_t block_size;
   uint32_t block_magic;     // floor(n / block_size) = (umulhi(n, magic) + n) >> shift
   int32_t block_shift;      //   for 0 <= n < 2^31 (division by an invariant integer)
