@@ -26,8 +26,8 @@
  * Conventions shared by every call
  *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
  *     allocates no device memory and keeps no state across calls except small
- *     host caches (per-device compute-unit count, recent automatic split
- *     choices, per-device scratch addresses) and the static device scratch
+ *     host caches (per-device compute-unit count, recent automatic split and
+ *     pairing choices, per-device scratch addresses) and the static device scratch
  *     of mocap_chunk_attn_noalloc (MOCAP_NOALLOC_SCRATCH_BYTES per device,
  *     part of the loaded library image, never allocated by a call).
  *   - Calls enqueue work on `stream` (a hipStream_t passed as void*; NULL is
