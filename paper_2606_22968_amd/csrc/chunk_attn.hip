@@ -10,12 +10,16 @@
 //     as the B operand of the score product.  All wavefronts of a workgroup
 //     share one KV head (GQA packing), so each K/V tile staged in LDS serves
 //     every query head of the group.
-//   * Causal balance: the workgroup's two units of four waves take row
-//     groups r and R-1-r of the same query heads, so every workgroup carries
-//     about the same number of (row, key) pairs.  Each wave follows its own
-//     key range: it stops computing after the last tile its rows see (the
-//     other unit's wave on its SIMD then has the SIMD alone) and treats the
-//     tiles all its rows see in full as unmasked.
+//   * Causal balance: the workgroup's two units of four waves take two row
+//     groups of the same query heads, r and R-1-r (mirrored, so every
+//     workgroup carries about the same number of (row, key) pairs) or two
+//     adjacent ones (when many workgroups per CU even out their lengths);
+//     the host picks per launch.  Each wave follows its own key range and
+//     treats the tiles all its rows see in full as unmasked.  In a mirrored
+//     pair, the last tiles only the longer row group sees are shared: the
+//     shorter group's wave stores its rows, takes over its partner's rows
+//     and computes the second 32-key half of each such tile while the
+//     partner computes the first; the two partial results meet in LDS.
 //   * K/V advance in tiles of 64 keys, copied global -> LDS directly
 //     (buffer_load_dwordx4 ... lds, no staging registers) into a 4-stage ring
 //     (128 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
@@ -53,6 +57,8 @@
 #include "internal.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace mocap {
 namespace {
@@ -220,10 +226,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   const int unit_rows = (kAttnWaves / 2 / hu) * kAttnWaveRows;
   const int uw = wave & 3;
   const int head = item.head0 + (uw % hu);
-  const int my_rg = (wave >> 2) == 0 ? item.row_group_a : item.row_group_b;
-  const int row0_unclamped = my_rg * unit_rows + (uw / hu) * kAttnWaveRows;
-  const bool wave_on = my_rg >= 0 && row0_unclamped < L;  // a wave whose rows all lie past L has nothing to do
-  const int row0 = max(my_rg, 0) * unit_rows + (uw / hu) * kAttnWaveRows;
+  const bool unit_b = (wave >> 2) != 0;
+  // First row of this wave slot in row group rg, and whether any of its rows lies before L.
+  auto slot_row0 = [&](int rg) { return max(rg, 0) * unit_rows + (uw / hu) * kAttnWaveRows; };
+  auto slot_on = [&](int rg) { return rg >= 0 && rg * unit_rows + (uw / hu) * kAttnWaveRows < L; };
+  const int my_rg = unit_b ? item.row_group_b : item.row_group_a;
+  const bool wave_on = slot_on(my_rg);  // a wave whose rows all lie past L has nothing to do
+  int row0 = slot_row0(my_rg);
   const int wg_row0 = item.row_group_a * unit_rows;
   const int wg_row_end = min(L, (max(item.row_group_a, item.row_group_b) + 1) * unit_rows);
 
@@ -253,20 +262,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     if (i < n_fast + n_head) return tile_begin;
     return fast_end + (i - n_fast - n_head);
   };
-  // This wave's share of the sequence: the first n_w positions (the tiles
-  // its rows see; tiles past them come last in the order above), and, among
+  // A wave's share of the sequence: the first n positions (the tiles its
+  // rows see; tiles past them come last in the order above), and, among
   // them, the tiles every one of its rows sees in full (unmasked).
-  const int w_tile_end = (min(hi, P + row0 + kAttnWaveRows) + kTileKeys - 1) / kTileKeys;
-  const int n_w = wave_on ? n_tiles - max(0, tile_end - w_tile_end) : 0;
-  const int w_full_end = min(hi, P + row0 + 1);
+  auto share_of = [&](int r0, bool on) {
+    const int w_tile_end = (min(hi, P + r0 + kAttnWaveRows) + kTileKeys - 1) / kTileKeys;
+    return on ? n_tiles - max(0, tile_end - w_tile_end) : 0;
+  };
+  const int n_w = share_of(row0, wave_on);
+  int w_full_end = min(hi, P + row0 + 1);
+  // Mirrored pairs leave the unit with the shorter row group idle on the
+  // last positions, which only the other unit's rows see.  When there are
+  // at least kHelpTiles of them, the wave of the shorter unit moves over to
+  // its partner's rows for those positions (the same wave slot of the other
+  // unit: same head, same SIMD): the partner computes the first 32-key half
+  // of each such tile, the helper the second, and the two partial results
+  // are merged through LDS at the end.  Both waves derive the same plan.
+  constexpr int kHelpTiles = 4;
+  const bool merge_wg = !p.pair_adjacent && item.row_group_b >= 0;
+  const int a_n_w = share_of(slot_row0(item.row_group_a), slot_on(item.row_group_a));
+  const int partner_row0 = slot_row0(item.row_group_b);
+  const int partner_n_w = share_of(partner_row0, slot_on(item.row_group_b));
+  const bool help = merge_wg && partner_n_w - a_n_w >= kHelpTiles;
+  const int help_from = a_n_w;
   auto masked_at = [&](int i) __attribute__((always_inline)) -> bool {
     const int t = seq_tile(i);
     return t * kTileKeys < lo || (t + 1) * kTileKeys > w_full_end;
   };
 
-  // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T).
+  // Q fragments of the current 32 rows (B operand of S^T = K Q^T).
   bf16x8 qf[KS];
-  {
+  auto load_q = [&]() __attribute__((always_inline)) {
     const int row = row0 + l32;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -276,7 +302,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         qf[ks] = bf16x8{};
       }
     }
-  }
+  };
+  load_q();
 
 
   const int64_t head_stride = (int64_t)D * p.block_size;
@@ -362,50 +389,54 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     return i1 > i0 ? (((1u << i1) - 1u) & ~((1u << i0) - 1u)) : 0u;
   };
 
-  // Pieces of one 64-key tile: scores (16 MFMAs), probabilities of each
-  // 32-key half (VALU), settle, P*V (16 MFMAs).
+  // Pieces of one 64-key tile.  NH = 2 (nh2): the whole tile -- scores (16
+  // MFMAs), probabilities of both 32-key halves, settle, P*V (16 MFMAs).
+  // NH = 1 (nh1): only the 32-key half h0 (8 + 8 MFMAs), when two waves
+  // share each tile's keys (their partial results are merged at the end).
   f32x16 s[2];
   uint32_t pk[2][2][8];  // [buffer][32-key half][packed pairs]: tile i uses buffer i % 2
   float rs[2], fs[2];  // per 32-key half: bf16 sum, fp32 sum
-  auto scores = [&](int i, bool masked) __attribute__((always_inline)) {
+  auto scores = [&](auto nh, int i, bool masked, int h0) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
     const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
-    const uint16_t* krow0 = kl + k_row_lo * D;
-    const uint16_t* krow1 = kl + (32 + k_row_lo) * D;
-    const int ksw0 = k_swizzle<D>(k_row_lo), ksw1 = k_swizzle<D>(32 + k_row_lo);
-    // The two 32-key halves are independent accumulation chains; their K
+    const int kr0 = h0 * 32 + k_row_lo, kr1 = 32 + k_row_lo;
+    const uint16_t* krow0 = kl + kr0 * D;
+    const uint16_t* krow1 = kl + kr1 * D;
+    const int ksw0 = k_swizzle<D>(kr0), ksw1 = k_swizzle<D>(kr1);
+    // The 32-key halves are independent accumulation chains; their K
     // fragments are read two k-steps ahead of the MFMAs that use them.
     auto kfrag = [&](const uint16_t* krow, int ksw, int ks) __attribute__((always_inline)) {
       return *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
     };
     bf16x8 a0[KS], a1[KS];
     a0[0] = kfrag(krow0, ksw0, 0);
-    a1[0] = kfrag(krow1, ksw1, 0);
+    if constexpr (NH == 2) a1[0] = kfrag(krow1, ksw1, 0);
     a0[1] = kfrag(krow0, ksw0, 1);
-    a1[1] = kfrag(krow1, ksw1, 1);
+    if constexpr (NH == 2) a1[1] = kfrag(krow1, ksw1, 1);
     s[0] = s[1] = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (ks + 2 < KS) {
         a0[ks + 2] = kfrag(krow0, ksw0, ks + 2);
-        a1[ks + 2] = kfrag(krow1, ksw1, ks + 2);
+        if constexpr (NH == 2) a1[ks + 2] = kfrag(krow1, ksw1, ks + 2);
       }
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[ks], qf[ks], s[0], 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], qf[ks], s[1], 0, 0, 0);
+      if constexpr (NH == 2) s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], qf[ks], s[1], 0, 0, 0);
     }
-    // Issue order: four fragment reads, then each MFMA followed by the next
-    // read, so reads stay two k-steps ahead of their MFMAs.
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);  // LDS reads
+    // Issue order: the first 2 * NH fragment reads, then each MFMA followed
+    // by the next read, so reads stay two k-steps ahead of their MFMAs.
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NH, 1);  // LDS reads
 #pragma unroll
-    for (int k = 0; k < 2 * KS; ++k) {
+    for (int k = 0; k < NH * KS; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // MFMA
-      if (k + 4 < 2 * KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      if (k + 2 * NH < NH * KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
     }
     if (masked) {
       // Hidden scores become -inf, so their probabilities are exactly 0.
       const int tstart = seq_tile(i) * kTileKeys;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const uint32_t vm = visible_bits(tstart + sb * 32 + half * 8);
+      for (int sb = 0; sb < NH; ++sb) {
+        const uint32_t vm = visible_bits(tstart + (h0 + sb) * 32 + half * 8);
 #pragma unroll
         for (int i2 = 0; i2 < 16; ++i2) {
           const int keep = __builtin_amdgcn_sbfe((int)vm, i2, 1);
@@ -414,10 +445,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       }
     }
   };
-  // Probabilities of both 32-key halves into buffer b and their row sums.
-  auto probs = [&](int b, float neg_m) __attribute__((always_inline)) {
+  // Probabilities of the NH halves into buffer b and their row sums.
+  auto probs = [&](auto nh, int b, float neg_m) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
+    for (int sb = 0; sb < NH; ++sb) {
       float fa = 0.f;
 #pragma unroll
       for (int i2 = 0; i2 < 16; i2 += 2) {
@@ -429,23 +461,25 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       fs[sb] = fa;
     }
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
+    for (int sb = 0; sb < NH; ++sb) {
       float acc = 0.f;
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc = dot2_bf16(pk[b][sb][j], ones, acc);
       rs[sb] = acc;
     }
+    if constexpr (NH == 1) rs[1] = fs[1] = 0.f;
   };
   // A row still without a reference exponent (m = -inf, exponent offset
   // +inf) has an infinite or NaN sum here, which sends it to the fresh branch.
-  auto settle = [&](int b) __attribute__((always_inline)) {
+  auto settle = [&](auto nh, int b) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
     const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
       const bool row_over = lane_pair_max(over ? 1.f : 0.f) > 0.f;
       // Largest score of the block (hidden ones are -inf).
       float mx = -INFINITY;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int sb = 0; sb < NH; ++sb)
 #pragma unroll
         for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, s[sb][i2]);
       mx = lane_pair_max(mx) * sl2;
@@ -460,41 +494,43 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
           f_run *= f;
         }
         m_run = mx;
-        probs(b, m_run == -INFINITY ? 0.f : -m_run);
+        probs(nh, b, m_run == -INFINITY ? 0.f : -m_run);
       }
     }
     l_run += rs[0] + rs[1];
     f_run += fs[0] + fs[1];
   };
-  auto pv = [&](int i, int b) __attribute__((always_inline)) {
+  auto pv = [&](auto nh, int i, int b, int h0) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
     auto vfrag = [&](int kst, int md) __attribute__((always_inline)) {
       const int vchunk = (kst * 2 + half) ^ v_row_sw;
       return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
     };
 #pragma unroll
-    for (int kst = 0; kst < 4; ++kst) {
-      const int sb = kst / 2, kk = kst % 2;
+    for (int kl = 0; kl < 2 * NH; ++kl) {
+      const int sb = kl / 2, kk = kl % 2;
       const bf16x8 pb = __builtin_bit_cast(
           bf16x8, u32x4{pk[b][sb][kk * 4], pk[b][sb][kk * 4 + 1], pk[b][sb][kk * 4 + 2], pk[b][sb][kk * 4 + 3]});
 #pragma unroll
       for (int md = 0; md < MD; ++md)
-        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(kst, md), pb, oacc[md], 0, 0, 0);
+        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(2 * h0 + kl, md), pb, oacc[md], 0, 0, 0);
     }
   };
   // Tile i's P*V (probabilities from buffer bo) with the next tile's
   // probabilities (into buffer bn) woven in: after each MFMA, the
-  // exponentials, packing and row sums of 32 / (4 * MD) score pairs.  V
-  // fragments are read two MFMAs ahead.  The scheduling barrier after each
-  // step keeps this order, which the compiler's scheduler would otherwise
-  // collapse into all MFMAs first.
-  auto pv_probs = [&](int i, int bo, int bn, float neg_m) __attribute__((always_inline)) {
+  // exponentials, packing and row sums of 8 * NH / (2 * NH * MD) score
+  // pairs.  V fragments are read two MFMAs ahead.  The scheduling barrier
+  // after each step keeps this order, which the compiler's scheduler would
+  // otherwise collapse into all MFMAs first.
+  auto pv_probs = [&](auto nh, int i, int bo, int bn, float neg_m, int h0) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
-    auto vfrag = [&](int kst, int md) __attribute__((always_inline)) {
-      const int vchunk = (kst * 2 + half) ^ v_row_sw;
+    auto vfrag = [&](int kl, int md) __attribute__((always_inline)) {
+      const int vchunk = ((2 * h0 + kl) * 2 + half) ^ v_row_sw;
       return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
     };
-    constexpr int NF = 4 * MD, AHEAD = 2, PAIRS = 16 / NF;
+    constexpr int NF = 2 * NH * MD, AHEAD = 2, NPAIRS = 8 * NH, PAIRS = NPAIRS / NF;
     bf16x8 vf[AHEAD + 1];
 #pragma unroll
     for (int k = 0; k < AHEAD; ++k) vf[k] = vfrag(k / MD, k % MD);
@@ -503,7 +539,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     // just before it.
     constexpr int LAG_PACK = 2, LAG_SUM = 4;
     float acc[2] = {0.f, 0.f}, facc[2] = {0.f, 0.f};
-    float ex[16][2];
+    float ex[NPAIRS][2];
     auto do_exp = [&](int pr) __attribute__((always_inline)) {
       const int nsb = pr / 8, j = pr % 8;
       ex[pr][0] = __builtin_amdgcn_exp2f(fmaf(s[nsb][2 * j], sl2, neg_m));
@@ -518,7 +554,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     };
 #pragma unroll
     for (int k = 0; k < NF; ++k) {
-      const int kst = k / MD, md = k % MD, sb = kst / 2, kk = kst % 2;
+      const int kl = k / MD, md = k % MD, sb = kl / 2, kk = kl % 2;
       if (k + AHEAD < NF) vf[(k + AHEAD) % (AHEAD + 1)] = vfrag((k + AHEAD) / MD, (k + AHEAD) % MD);
       const bf16x8 pb = __builtin_bit_cast(
           bf16x8, u32x4{pk[bo][sb][kk * 4], pk[bo][sb][kk * 4 + 1], pk[bo][sb][kk * 4 + 2], pk[bo][sb][kk * 4 + 3]});
@@ -533,8 +569,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int pr = 16; pr < 16 + LAG_SUM; ++pr) {
-      if (pr - LAG_PACK < 16) do_pack(pr - LAG_PACK);
+    for (int pr = NPAIRS; pr < NPAIRS + LAG_SUM; ++pr) {
+      if (pr - LAG_PACK < NPAIRS) do_pack(pr - LAG_PACK);
       do_sum(pr - LAG_SUM);
     }
     rs[0] = acc[0];
@@ -552,13 +588,73 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // Position i of the sequence (probabilities into buffer b): scores, then
   // the previous tile's P*V with this tile's probabilities woven in, so one
   // wave keeps both the matrix and the vector units busy.
-  auto step = [&](int i, int b) __attribute__((always_inline)) {
+  auto step = [&](auto nh, int i, int b, int h0) __attribute__((always_inline)) {
     barrier_k(i);
-    scores(i, masked_at(i));
-    pv_probs(i - 1, b ^ 1, b, -m_run);
-    settle(b);
+    scores(nh, i, masked_at(i), h0);
+    pv_probs(nh, i - 1, b ^ 1, b, -m_run, h0);
+    settle(nh, b);
+  };
+  // Positions [from, to) of the sequence, meeting their barriers: the first
+  // tile's scores and probabilities, the woven steps, and the last P*V.
+  auto run_range = [&](auto nh, int from, int to, int h0) __attribute__((always_inline)) {
+    barrier_k(from);
+    scores(nh, from, masked_at(from), h0);
+    probs(nh, 0, -m_run);
+    settle(nh, 0);
+    for (int i = from + 1; i < to; i += 2) {
+      step(nh, i, 1, h0);
+      if (i + 1 < to) step(nh, i + 1, 0, h0);
+    }
+    if ((to - 1 - from) & 1) {  // the last tile's probabilities are in buffer 1
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
+    }
+    pv(nh, to - 1, 0, h0);
+  };
+  // O and LSE of the current rows (or their split partials).
+  const bool split = p.n_ranges > 1;
+  auto store_outputs = [&]() __attribute__((always_inline)) {
+    const float l_tot = lane_pair_sum(l_run);
+    const float f_tot = lane_pair_sum(f_run);
+    const int row = row0 + l32;
+    if (row < L) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      const float row_lse = f_tot > 0.f ? (m_run + log2f(f_tot)) * kLn2 : -INFINITY;
+      if (!split) {
+        uint16_t* orow = p.o + ((int64_t)row * p.h_q + head) * D;
+#pragma unroll
+        for (int md = 0; md < MD; ++md) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            bf16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (__bf16)(oacc[md][j * 4 + e] * inv);
+            *reinterpret_cast<bf16x4*>(orow + md * 32 + j * 8 + half * 4) = v;
+          }
+        }
+        if (half == 0) p.lse[(int64_t)head * L + row] = row_lse;
+      } else {
+        const int64_t base = ((int64_t)item.range * p.h_q + head) * L + row;
+        float* orow = p.ws_o + base * D;
+#pragma unroll
+        for (int md = 0; md < MD; ++md) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = oacc[md][j * 4 + e] * inv;
+            *reinterpret_cast<f32x4*>(orow + md * 32 + j * 8 + half * 4) = v;
+          }
+        }
+        if (half == 0) p.ws_lse[base] = row_lse;
+      }
+    }
   };
 
+  const std::integral_constant<int, 2> nh2;
+  const std::integral_constant<int, 1> nh1;
   if (n_tiles > 0) {
     // Without this, values the first tile derives from these (its masks, its
     // LDS addresses) are computed once ahead of the loop and then occupy
@@ -566,67 +662,79 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     asm volatile("" : "+s"(lo), "+s"(hi), "+v"(k_row_lo), "+v"(v_row_sw));
     issue_seq(0);
     if (n_tiles > 1) issue_seq(1);
-    barrier_k(0);
-    if (n_w > 0) {
-      scores(0, masked_at(0));
-      probs(0, -m_run);
-      settle(0);
+    // Whole tiles: this wave's own positions, or, when the unit pair
+    // shares the last positions, the positions before them.  Then the
+    // shared positions: the helped wave keeps its rows and takes the first
+    // 32-key half of each tile; the helping wave stores its own rows and
+    // takes the second half for its partner's rows.  One copy of each loop
+    // serves every wave.
+    const int full_end = help ? help_from : n_w;
+    int done = 0;  // positions whose barrier this wave has met
+    if (full_end > 0) {
+      run_range(nh2, 0, full_end, 0);
+      done = full_end;
     }
-    // The wave computes positions [0, n_w), finishes the P*V of its last
-    // tile, then only copies tiles and meets the remaining barriers (every
-    // wave meets barrier k once, in order, for every k < n_tiles).
-    for (int i = 1; i < n_w; i += 2) {
-      step(i, 1);
-      if (i + 1 < n_w) step(i + 1, 0);
-    }
-    if (n_w > 0) {
-      if ((n_w - 1) & 1) {  // the last tile's probabilities are in buffer 1
+    if (help) {
+      if (!unit_b) {
+        if (full_end > 0) store_outputs();
+        row0 = partner_row0;
+        w_full_end = min(hi, P + row0 + 1);
+        load_q();
+        m_run = -INFINITY;
+        l_run = f_run = 0.f;
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
+        for (int md = 0; md < MD; ++md) oacc[md] = f32x16{};
       }
-      pv(n_w - 1, 0);
+      run_range(nh1, help_from, partner_n_w, unit_b ? 0 : 1);
+      done = partner_n_w;
     }
-    for (int i = max(n_w, 1); i < n_tiles; ++i) barrier_k(i);
+    if (done == 0) {
+      barrier_k(0);
+      done = 1;
+    }
+    for (int i = done; i < n_tiles; ++i) barrier_k(i);
   }
 
-  const bool split = p.n_ranges > 1;
-  const float l_tot = lane_pair_sum(l_run);
-  const float f_tot = lane_pair_sum(f_run);
-  const int row = row0 + l32;
-  if (wave_on && row < L) {
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float row_lse = f_tot > 0.f ? (m_run + log2f(f_tot)) * kLn2 : -INFINITY;
-    if (!split) {
-      uint16_t* orow = p.o + ((int64_t)row * p.h_q + head) * D;
+  if (merge_wg) {
+    // The helping wave hands its partial (O, m and both sums of the
+    // partner's rows over the second key halves) to the partner through LDS,
+    // which no tile occupies any more.
+    constexpr int NV = MD * 16;
+    float* mb = reinterpret_cast<float*>(lds) + uw * (NV + 3) * 64;
+    lds_barrier();
+    if (help && !unit_b) {
 #pragma unroll
-      for (int md = 0; md < MD; ++md) {
+      for (int md = 0; md < MD; ++md)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(mb + ((md * 4 + j) * 64 + lane) * 4) =
+              f32x4{oacc[md][j * 4], oacc[md][j * 4 + 1], oacc[md][j * 4 + 2], oacc[md][j * 4 + 3]};
+      mb[NV * 64 + lane] = m_run;
+      mb[NV * 64 + 64 + lane] = l_run;
+      mb[NV * 64 + 128 + lane] = f_run;
+    }
+    lds_barrier();
+    if (help && unit_b) {
+      const float m_a = mb[NV * 64 + lane];
+      const float m = fmaxf(m_run, m_a);
+      const float cb = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m);
+      const float ca = m_a == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_a - m);
+#pragma unroll
+      for (int md = 0; md < MD; ++md)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          bf16x4 v;
+          const f32x4 o_a = *reinterpret_cast<const f32x4*>(mb + ((md * 4 + j) * 64 + lane) * 4);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (__bf16)(oacc[md][j * 4 + e] * inv);
-          *reinterpret_cast<bf16x4*>(orow + md * 32 + j * 8 + half * 4) = v;
+          for (int e = 0; e < 4; ++e) oacc[md][j * 4 + e] = oacc[md][j * 4 + e] * cb + o_a[e] * ca;
         }
-      }
-      if (half == 0) p.lse[(int64_t)head * L + row] = row_lse;
-    } else {
-      const int64_t base = ((int64_t)item.range * p.h_q + head) * L + row;
-      float* orow = p.ws_o + base * D;
-#pragma unroll
-      for (int md = 0; md < MD; ++md) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          f32x4 v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = oacc[md][j * 4 + e] * inv;
-          *reinterpret_cast<f32x4*>(orow + md * 32 + j * 8 + half * 4) = v;
-        }
-      }
-      if (half == 0) p.ws_lse[base] = row_lse;
+      l_run = l_run * cb + mb[NV * 64 + 64 + lane] * ca;
+      f_run = f_run * cb + mb[NV * 64 + 128 + lane] * ca;
+      m_run = m;
     }
   }
+  // Waves with rows left to write: their own (no help), or the partner's
+  // merged rows (the wave that was helped); a helping wave stored its own.
+  if (help ? unit_b : wave_on) store_outputs();
 #endif  // __HIP_DEVICE_COMPILE__
 }
 

@@ -1,6 +1,10 @@
 """Both pairings of row groups inside an attention workgroup (mirrored q with
 R-1-q, adjacent 2q with 2q+1), forced through MOCAP_PAIRING, against the
-oracle.  The library normally picks one per launch from its time model."""
+oracle.  The library normally picks one per launch from its time model.
+Mirrored pairs whose row groups differ by at least four key tiles share
+their last tiles between the two waves of a SIMD (each takes one 32-key
+half, the partial results are merged in LDS); the long single chunks below
+make most pairs do so."""
 import pytest
 
 from helpers import check_chunks, run_gpu, say
@@ -14,6 +18,8 @@ pytestmark = pytest.mark.gpu
     (32, 8, 128, [1536, 768], 0),              # 12 / 6 row groups, automatic split
     (8, 2, 64, [5, 300, 211, 129], 3),         # odd row-group counts, forced split
     (12, 4, 128, [640, 383], 1),               # GQA group 3: one head per unit
+    (4, 1, 128, [2048], 0),                    # one causal triangle, 16 mirrored pairs
+    (3, 1, 64, [1500, 700], 2),                # one head per unit, head_dim 64, split prefix
 ])
 def test_pairing_matches_oracle(gpu, oracle_lib, monkeypatch, mode, h_q, h_kv, d, lengths, splits):
     monkeypatch.setenv("MOCAP_PAIRING", mode)
