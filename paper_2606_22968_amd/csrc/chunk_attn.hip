@@ -25,12 +25,15 @@
 //     (128 KiB at head_dim 128), prefetched two tiles ahead, one workgroup
 //     barrier per tile.  Even tiles are copied by waves 0-3 and odd tiles by
 //     waves 4-7, so each wave computes a tile's addresses every other tile.
-//   * Software pipelining inside each wavefront: tile k's scores are followed
-//     by tile k-1's P*V product with tile k's exp/pack/row-sum work woven in
-//     at a fixed ratio (two scores per MFMA, four at head_dim 64), so the
-//     matrix and vector units work side by side.  The probabilities alternate
-//     between two register buffers.  LDS operand fragments are read two or
-//     more MFMAs ahead.
+//   * Software pipelining inside each wavefront, in two complementary orders
+//     for the two waves of a SIMD.  Waves 0-3: tile k's scores (MFMAs only),
+//     then tile k-1's P*V with tile k's exp/pack/row-sum work woven in at a
+//     fixed ratio (two scores per MFMA, four at head_dim 64); the
+//     probabilities alternate between two register buffers.  Waves 4-7: tile
+//     k's scores with tile k-1's softmax work woven in (at raised wave
+//     priority), then tile k-1's P*V alone.  So while one wave of a SIMD
+//     interleaves vector work with its MFMAs, the other mostly issues MFMAs.
+//     LDS operand fragments are read two or more MFMAs ahead.
 //   * Scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: a lane's accumulator then holds one query and
 //     16 keys, so row statistics need one cross-half exchange
@@ -396,7 +399,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   f32x16 s[2];
   uint32_t pk[2][2][8];  // [buffer][32-key half][packed pairs]: tile i uses buffer i % 2
   float rs[2], fs[2];  // per 32-key half: bf16 sum, fp32 sum
-  auto scores = [&](auto nh, int i, bool masked, int h0) __attribute__((always_inline)) {
+  auto scores = [&](auto nh, int i, bool masked, int h0, f32x16* s) __attribute__((always_inline)) {
     constexpr int NH = decltype(nh)::value;
     const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
     const int kr0 = h0 * 32 + k_row_lo, kr1 = 32 + k_row_lo;
@@ -445,16 +448,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
       }
     }
   };
-  // Probabilities of the NH halves into buffer b and their row sums.
-  auto probs = [&](auto nh, int b, float neg_m) __attribute__((always_inline)) {
+  // Probabilities of the NH halves of scores ss into buffer b and their row sums.
+  auto probs = [&](auto nh, const f32x16* ss, int b, float neg_m) __attribute__((always_inline)) {
     constexpr int NH = decltype(nh)::value;
 #pragma unroll
     for (int sb = 0; sb < NH; ++sb) {
       float fa = 0.f;
 #pragma unroll
       for (int i2 = 0; i2 < 16; i2 += 2) {
-        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2], sl2, neg_m));
-        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i2 + 1], sl2, neg_m));
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(ss[sb][i2], sl2, neg_m));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(ss[sb][i2 + 1], sl2, neg_m));
         pk[b][sb][i2 / 2] = pack_bf16x2(e0, e1);
         fa += e0 + e1;
       }
@@ -471,7 +474,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   };
   // A row still without a reference exponent (m = -inf, exponent offset
   // +inf) has an infinite or NaN sum here, which sends it to the fresh branch.
-  auto settle = [&](auto nh, int b) __attribute__((always_inline)) {
+  auto settle = [&](auto nh, const f32x16* ss, int b) __attribute__((always_inline)) {
     constexpr int NH = decltype(nh)::value;
     const bool over = !(rs[0] <= kSumLimit) || !(rs[1] <= kSumLimit);
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
@@ -481,7 +484,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
 #pragma unroll
       for (int sb = 0; sb < NH; ++sb)
 #pragma unroll
-        for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, s[sb][i2]);
+        for (int i2 = 0; i2 < 16; ++i2) mx = fmaxf(mx, ss[sb][i2]);
       mx = lane_pair_max(mx) * sl2;
       if (row_over) {
         // A row with nothing accumulated yet (m = -inf) just takes its
@@ -494,27 +497,33 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
           f_run *= f;
         }
         m_run = mx;
-        probs(nh, b, m_run == -INFINITY ? 0.f : -m_run);
+        probs(nh, ss, b, m_run == -INFINITY ? 0.f : -m_run);
       }
     }
     l_run += rs[0] + rs[1];
     f_run += fs[0] + fs[1];
   };
+  // Tile i's P*V alone (probabilities from buffer b), V fragments read
+  // AHEAD MFMAs before their use.
   auto pv = [&](auto nh, int i, int b, int h0) __attribute__((always_inline)) {
     constexpr int NH = decltype(nh)::value;
     const uint16_t* vl = lds + (i % STAGES) * BUF_ELEMS + K_ELEMS;
-    auto vfrag = [&](int kst, int md) __attribute__((always_inline)) {
-      const int vchunk = (kst * 2 + half) ^ v_row_sw;
+    auto vfrag = [&](int kl, int md) __attribute__((always_inline)) {
+      const int vchunk = ((2 * h0 + kl) * 2 + half) ^ v_row_sw;
       return *reinterpret_cast<const bf16x8*>(vl + (md * 32 + l32) * kTileKeys + (vchunk << 3));
     };
+    constexpr int NF = 2 * NH * MD, AHEAD = 3;
+    bf16x8 vf[AHEAD + 1];
 #pragma unroll
-    for (int kl = 0; kl < 2 * NH; ++kl) {
-      const int sb = kl / 2, kk = kl % 2;
+    for (int k = 0; k < AHEAD; ++k) vf[k] = vfrag(k / MD, k % MD);
+#pragma unroll
+    for (int k = 0; k < NF; ++k) {
+      const int kl = k / MD, md = k % MD, sb = kl / 2, kk = kl % 2;
+      if (k + AHEAD < NF) vf[(k + AHEAD) % (AHEAD + 1)] = vfrag((k + AHEAD) / MD, (k + AHEAD) % MD);
       const bf16x8 pb = __builtin_bit_cast(
           bf16x8, u32x4{pk[b][sb][kk * 4], pk[b][sb][kk * 4 + 1], pk[b][sb][kk * 4 + 2], pk[b][sb][kk * 4 + 3]});
-#pragma unroll
-      for (int md = 0; md < MD; ++md)
-        oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(2 * h0 + kl, md), pb, oacc[md], 0, 0, 0);
+      oacc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k % (AHEAD + 1)], pb, oacc[md], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Tile i's P*V (probabilities from buffer bo) with the next tile's
@@ -590,17 +599,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
   // wave keeps both the matrix and the vector units busy.
   auto step = [&](auto nh, int i, int b, int h0) __attribute__((always_inline)) {
     barrier_k(i);
-    scores(nh, i, masked_at(i), h0);
+    scores(nh, i, masked_at(i), h0, s);
     pv_probs(nh, i - 1, b ^ 1, b, -m_run, h0);
-    settle(nh, b);
+    settle(nh, s, b);
   };
   // Positions [from, to) of the sequence, meeting their barriers: the first
   // tile's scores and probabilities, the woven steps, and the last P*V.
   auto run_range = [&](auto nh, int from, int to, int h0) __attribute__((always_inline)) {
     barrier_k(from);
-    scores(nh, from, masked_at(from), h0);
-    probs(nh, 0, -m_run);
-    settle(nh, 0);
+    scores(nh, from, masked_at(from), h0, s);
+    probs(nh, s, 0, -m_run);
+    settle(nh, s, 0);
     for (int i = from + 1; i < to; i += 2) {
       step(nh, i, 1, h0);
       if (i + 1 < to) step(nh, i + 1, 0, h0);
@@ -612,6 +621,123 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
         for (int j = 0; j < 8; ++j) pk[0][sb][j] = pk[1][sb][j];
     }
     pv(nh, to - 1, 0, h0);
+  };
+  // The order of the other unit (waves 4-7; wave w and w + 4 share a SIMD):
+  // tile i's scores with tile i-1's exponentials, packing and row sums woven
+  // in after each MFMA, then tile i-1's P*V alone.  One wave of each SIMD is
+  // then in an MFMA-only phase while the other interleaves the softmax.
+  f32x16 sc[2][2];  // [tile parity][32-key half]
+  auto mask_scores = [&](auto nh, int i, f32x16* ss) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
+    const int tstart = seq_tile(i) * kTileKeys;
+#pragma unroll
+    for (int sb = 0; sb < NH; ++sb) {
+      const uint32_t vm = visible_bits(tstart + sb * 32 + half * 8);
+#pragma unroll
+      for (int i2 = 0; i2 < 16; ++i2) {
+        const int keep = __builtin_amdgcn_sbfe((int)vm, i2, 1);
+        ss[sb][i2] = __int_as_float((__float_as_int(ss[sb][i2]) & keep) | (~keep & (int)0xFF800000u));
+      }
+    }
+  };
+  // Tile i's scores into sn with the probabilities of tile i-1 (scores sp,
+  // masked here first when tile i-1 straddles an edge) woven in.
+  auto scores_probs = [&](auto nh, int i, f32x16* sn, f32x16* sp, float neg_m) __attribute__((always_inline)) {
+    constexpr int NH = decltype(nh)::value;
+    if (masked_at(i - 1)) mask_scores(nh, i - 1, sp);
+    const uint16_t* kl = lds + (i % STAGES) * BUF_ELEMS;
+    const int kr0 = k_row_lo, kr1 = 32 + k_row_lo;
+    const uint16_t* krow0 = kl + kr0 * D;
+    const uint16_t* krow1 = kl + kr1 * D;
+    const int ksw0 = k_swizzle<D>(kr0), ksw1 = k_swizzle<D>(kr1);
+    // MFMA k uses half k % NH at k-step k / NH; its K fragment is read AHEAD
+    // MFMAs earlier.
+    constexpr int NF = NH * KS, AHEAD = 3, NPAIRS = 8 * NH, PAIRS = NPAIRS / NF;
+    static_assert(PAIRS * NF == NPAIRS, "whole score pairs per MFMA");
+    auto kfrag = [&](int k) __attribute__((always_inline)) {
+      const int sb = k % NH, ks = k / NH;
+      const uint16_t* krow = sb == 0 ? krow0 : krow1;
+      const int ksw = sb == 0 ? ksw0 : ksw1;
+      return *reinterpret_cast<const bf16x8*>(krow + (((ks * 2 + half) ^ ksw) << 3));
+    };
+    bf16x8 kf[AHEAD + 1];
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) kf[k] = kfrag(k);
+    constexpr int LAG_PACK = 2, LAG_SUM = 4;
+    float acc[2] = {0.f, 0.f}, facc[2] = {0.f, 0.f};
+    float ex[NPAIRS][2];
+    auto do_exp = [&](int pr) __attribute__((always_inline)) {
+      const int psb = pr / 8, j = pr % 8;
+      ex[pr][0] = __builtin_amdgcn_exp2f(fmaf(sp[psb][2 * j], sl2, neg_m));
+      ex[pr][1] = __builtin_amdgcn_exp2f(fmaf(sp[psb][2 * j + 1], sl2, neg_m));
+    };
+    auto do_pack = [&](int pr) __attribute__((always_inline)) {
+      pk[0][pr / 8][pr % 8] = pack_bf16x2(ex[pr][0], ex[pr][1]);
+    };
+    auto do_sum = [&](int pr) __attribute__((always_inline)) {
+      acc[pr / 8] = dot2_bf16(pk[0][pr / 8][pr % 8], ones, acc[pr / 8]);
+      facc[pr / 8] += ex[pr][0] + ex[pr][1];
+    };
+    sn[0] = sn[1] = f32x16{};
+#pragma unroll
+    for (int k = 0; k < NF; ++k) {
+      const int sb = k % NH, ks = k / NH;
+      if (k + AHEAD < NF) kf[(k + AHEAD) % (AHEAD + 1)] = kfrag(k + AHEAD);
+      sn[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k % (AHEAD + 1)], qf[ks], sn[sb], 0, 0, 0);
+#pragma unroll
+      for (int q = 0; q < PAIRS; ++q) {
+        const int pr = k * PAIRS + q;
+        do_exp(pr);
+        if (pr >= LAG_PACK) do_pack(pr - LAG_PACK);
+        if (pr >= LAG_SUM) do_sum(pr - LAG_SUM);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int pr = NPAIRS; pr < NPAIRS + LAG_SUM; ++pr) {
+      if (pr - LAG_PACK < NPAIRS) do_pack(pr - LAG_PACK);
+      do_sum(pr - LAG_SUM);
+    }
+    rs[0] = acc[0];
+    rs[1] = acc[1];
+    fs[0] = facc[0];
+    fs[1] = facc[1];
+  };
+  // Position i in the other unit's order: tile i's scores (into sn) with the
+  // probabilities of tile i-1 (scores sp) woven in, then tile i-1's P*V.  The
+  // woven phase runs at raised wave priority, so its MFMAs issue as soon as
+  // their operands are ready and the partner wave's MFMA-only phase fills the
+  // gaps; at equal priority the older partner's back-to-back MFMAs held the
+  // matrix unit and stalled this wave's in-order stream.
+  auto step_b = [&](int i, f32x16* sn, f32x16* sp) __attribute__((always_inline)) {
+    const std::integral_constant<int, 2> nh;
+    barrier_k(i);
+    __builtin_amdgcn_s_setprio(1);
+    scores_probs(nh, i, sn, sp, -m_run);
+    __builtin_amdgcn_s_setprio(0);
+    settle(nh, sp, 0);
+    pv(nh, i - 1, 0, 0);
+  };
+  // Positions [from, to) in the other unit's order (whole tiles).
+  auto run_range_b = [&](int from, int to) __attribute__((always_inline)) {
+    const std::integral_constant<int, 2> nh;
+    barrier_k(from);
+    scores(nh, from, false, 0, sc[0]);
+    for (int i = from + 1; i < to; i += 2) {
+      step_b(i, sc[1], sc[0]);
+      if (i + 1 < to) step_b(i + 1, sc[0], sc[1]);
+    }
+    // The last tile's scores are in sc[1] after an odd number of steps.
+    if ((to - 1 - from) & 1) {
+      if (masked_at(to - 1)) mask_scores(nh, to - 1, sc[1]);
+      probs(nh, sc[1], 0, -m_run);
+      settle(nh, sc[1], 0);
+    } else {
+      if (masked_at(to - 1)) mask_scores(nh, to - 1, sc[0]);
+      probs(nh, sc[0], 0, -m_run);
+      settle(nh, sc[0], 0);
+    }
+    pv(nh, to - 1, 0, 0);
   };
   // O and LSE of the current rows (or their split partials).
   const bool split = p.n_ranges > 1;
@@ -671,7 +797,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     const int full_end = help ? help_from : n_w;
     int done = 0;  // positions whose barrier this wave has met
     if (full_end > 0) {
-      run_range(nh2, 0, full_end, 0);
+      if (unit_b) {
+        run_range_b(0, full_end);
+      } else {
+        run_range(nh2, 0, full_end, 0);
+      }
       done = full_end;
     }
     if (help) {
