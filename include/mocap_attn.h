@@ -465,10 +465,7 @@ mocap_status mocap_lbcp_refine_e2e(int64_t seq_len, int32_t num_chunks, int32_t 
  * on different streams, or from different threads without ordering -- race
  * on the scratch; order them on one stream.  The first call on a device
  * looks up the scratch's device address (hipGetSymbolAddress) with that
- * device current; a failure returns MOCAP_ERR_HIP.  (At head_dim 128 the
- * attention kernel also spills a few registers to per-lane private memory,
- * 64 bytes per lane, which the HIP runtime provides for every kernel launch;
- * no call of this library allocates it.)
+ * device current; a failure returns MOCAP_ERR_HIP.
  */
 mocap_status mocap_chunk_attn_noalloc(const mocap_kv_store* kv, const int32_t* block_table, int32_t n_table,
                                       const void* q, int64_t prefix_len, int32_t chunk_len, int32_t h_q,

@@ -652,7 +652,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     const int ksw0 = k_swizzle<D>(kr0), ksw1 = k_swizzle<D>(kr1);
     // MFMA k uses half k % NH at k-step k / NH; its K fragment is read AHEAD
     // MFMAs earlier.
-    constexpr int NF = NH * KS, AHEAD = 3, NPAIRS = 8 * NH, PAIRS = NPAIRS / NF;
+    constexpr int NF = NH * KS, AHEAD = 2, NPAIRS = 8 * NH, PAIRS = NPAIRS / NF;
     static_assert(PAIRS * NF == NPAIRS, "whole score pairs per MFMA");
     auto kfrag = [&](int k) __attribute__((always_inline)) {
       const int sb = k % NH, ks = k / NH;
@@ -729,14 +729,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void chunk_attn_kernel(const AttnL
     }
     // The last tile's scores are in sc[1] after an odd number of steps.
     if ((to - 1 - from) & 1) {
-      if (masked_at(to - 1)) mask_scores(nh, to - 1, sc[1]);
-      probs(nh, sc[1], 0, -m_run);
-      settle(nh, sc[1], 0);
-    } else {
-      if (masked_at(to - 1)) mask_scores(nh, to - 1, sc[0]);
-      probs(nh, sc[0], 0, -m_run);
-      settle(nh, sc[0], 0);
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) sc[0][sb] = sc[1][sb];
     }
+    if (masked_at(to - 1)) mask_scores(nh, to - 1, sc[0]);
+    probs(nh, sc[0], 0, -m_run);
+    settle(nh, sc[0], 0);
     pv(nh, to - 1, 0, 0);
   };
   // O and LSE of the current rows (or their split partials).
