@@ -22,7 +22,7 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # MFMA results in VGPRs: the score accumulators feed the softmax VALU work
-    # directly; read-only MFMA operands (the Q fragments) go to AGPRs.
+    # directly, with no copies out of accumulation registers.
     "-mllvm", "-amdgpu-mfma-vgpr-form=true",
     "-Wno-unused-command-line-argument",
     f"-I{INCLUDE}", f"-I{CSRC}",
